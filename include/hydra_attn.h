@@ -1,0 +1,139 @@
+/*
+ * hydra_attn.h -- one context-parallel (CP) rank's attention share on AMD MI355X (gfx950).
+ *
+ * What the library computes (arxiv 2609.34318, "HyDra"):
+ *   - Documents are packed into one window and attention is masked across their
+ *     boundaries (Sec. 2.2): a query at global position p attends to the keys of its
+ *     own document at positions <= p (causal, the diagonal included).
+ *   - A CP degree P is factored into an inner Ulysses group over heads and an outer
+ *     ring over the sequence, P = cp_u * cp_r (Sec. 5.2.1, Eq. (usp)).  A rank therefore
+ *     holds h / cp_u heads ("n_heads" below) and a chunk of the sequence; K/V chunks
+ *     circulate around the ring (Sec. 2.1, Sec. 3.5) and each ring step is one call here.
+ *   - Every step yields a partial output plus its log-sum-exp; partials combine exactly
+ *     as in standard ring CP (Sec. 5.2.2, last paragraph): hydra_lse_merge.
+ *   - Under MLA every head has its own K and V (Sec. 1); this library supports
+ *     d_qk = 192 and d_v = 128.
+ *
+ * Conventions shared by every call:
+ *   - Tensors are token-major and contiguous: X[token][head][dim], last dim fastest.
+ *     bf16 tensors are passed as raw 16-bit patterns.  LSE and D are [head][token] fp32,
+ *     natural logarithm.  "Token" is the rank-local row index; its global position comes
+ *     from the chunk's segments (hydra_chunk_t).
+ *   - Device pointers unless marked HOST.  Every device pointer must be 16-byte aligned.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Compute calls enqueue work
+ *     and return; kernel faults surface at the caller's next synchronisation.
+ *   - Compute calls never allocate device memory.  They upload a small work plan into the
+ *     caller's workspace with hipMemcpyAsync from host memory; that upload may wait for
+ *     work already queued on `stream`.
+ *   - The caller owns every buffer.  The library keeps no pointer after a call returns.
+ *   - All arguments are validated on the host before any HIP call; on error nothing is
+ *     written and no HIP call is made.  No C++ exception crosses this interface.
+ *   - Calls are thread-safe; two calls that write the same buffers must not overlap.
+ */
+#ifndef HYDRA_ATTN_H
+#define HYDRA_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes (returned as int). */
+#define HYDRA_OK                 0
+#define HYDRA_ERR_INVALID       -1  /* malformed argument: sizes, cu_seqlens, segments, NULL */
+#define HYDRA_ERR_UNSUPPORTED   -2  /* well-formed but not supported (d_qk != 192, d_v != 128) */
+#define HYDRA_ERR_ALIGN         -3  /* a device pointer is not 16-byte aligned */
+#define HYDRA_ERR_WORKSPACE     -4  /* workspace NULL or smaller than hydra_workspace_size() */
+#define HYDRA_ERR_HIP           -5  /* a HIP runtime call or kernel launch failed */
+
+#define HYDRA_MAX_SEGS 4
+
+/* A chunk of the packed sequence held by this rank: up to HYDRA_MAX_SEGS segments of
+ * consecutive global positions, laid out one after another as local rows.  One segment
+ * is a contiguous ring chunk; two segments express a zigzag (head + tail) chunk.
+ * Segments must lie inside [0, cu_seqlens[n_docs]); lengths may be 0. */
+typedef struct {
+  int32_t n_segs;                   /* 0..HYDRA_MAX_SEGS                                 */
+  int32_t start[HYDRA_MAX_SEGS];    /* global position of the segment's first token      */
+  int32_t len[HYDRA_MAX_SEGS];      /* tokens in the segment                              */
+} hydra_chunk_t;
+
+/* One ring step of one rank (Sec. 5.2.1: per-rank Q chunk, KV chunk, document boundaries,
+ * chunk global offsets, head shard). */
+typedef struct {
+  int32_t n_heads;                  /* head shard on this rank, h / cp_u; > 0            */
+  int32_t d_qk;                     /* must be 192                                       */
+  int32_t d_v;                      /* must be 128                                       */
+  float   softmax_scale;            /* <= 0 selects 1/sqrt(d_qk)                         */
+  const int32_t* cu_seqlens;        /* HOST int32[n_docs+1]: document boundaries in global
+                                       positions, cu[0] = 0, nondecreasing; read only
+                                       during the call                                   */
+  int32_t n_docs;                   /* >= 1                                              */
+  hydra_chunk_t q;                  /* this rank's query chunk                           */
+  hydra_chunk_t kv;                 /* this ring step's key/value chunk                  */
+} hydra_problem_t;
+
+/* Bytes of device workspace the compute calls need for `p` (host only, no GPU needed).
+ * Returns 0 if `p` is invalid. */
+size_t hydra_workspace_size(const hydra_problem_t* p);
+
+/* Forward partial of one ring step (Sec. 5.2.2; Sec. 2.2 for the masking):
+ *   q [Nq][H][192] bf16, k [Nk][H][192] bf16, v [Nk][H][128] bf16   (inputs)
+ *   o_part  [Nq][H][128] fp32   softmax(QK^T * scale, masked) V over this chunk's keys
+ *   lse_part [H][Nq] fp32       natural-log sum of exp of the visible scores
+ *   o_part_bf16: NULL, or [Nq][H][128] bf16 that also receives O (for a ring of one step,
+ *                whose partial is already final)
+ * A row that sees no key of this chunk gets O = 0 and LSE = -inf (the merge identity).
+ * Every row of o_part and lse_part is written. */
+int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                   float* o_part, float* lse_part, void* o_part_bf16,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward of one ring step, given the FINAL merged output and LSE of the rows (the same
+ * function is differentiated at every step):
+ *   o_final [Nq][H][128] bf16, lse_final [H][Nq] fp32, d_o [Nq][H][128] bf16
+ *   dq_acc [Nq][H][192] fp32 += this step's dQ        (caller zero-initialises once)
+ *   dk_acc [Nk][H][192] fp32 += dK of this KV chunk   from this rank's queries
+ *   dv_acc [Nk][H][128] fp32 += dV of this KV chunk   from this rank's queries
+ * The three gradient buffers must not overlap each other or the inputs. */
+int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                   const void* o_final, const float* lse_final, const void* d_o,
+                   float* dq_acc, float* dk_acc, float* dv_acc,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Exact merge of two partials of the same rows (ring CP, Sec. 5.2.2):
+ *   L = log(e^La + e^Lb),  O = e^(La-L) O_a + e^(Lb-L) O_b, in place into (o_acc, lse_acc).
+ * (0, -inf) is the identity; two empty rows stay (0, -inf) with no NaN.
+ *   o_acc/o_part [n_rows][n_heads][d_v] fp32, lse_acc/lse_part [n_heads][n_rows] fp32.
+ *   o_out_bf16: NULL, or [n_rows][n_heads][d_v] bf16 that also receives the merged O.
+ * d_v must be 128.  n_rows = 0 is a no-op. */
+int hydra_lse_merge(int64_t n_rows, int32_t n_heads, int32_t d_v,
+                    float* o_acc, float* lse_acc, const float* o_part, const float* lse_part,
+                    void* o_out_bf16, void* stream);
+
+/* Text for a status code (static storage). */
+const char* hydra_strerror(int status);
+
+/* Exact number of visible (query, key) pairs per head for `p` (host only).  The
+ * benchmark's FLOP count is this times 2*(d_qk+d_v) forward and 2*(3*d_qk+2*d_v)
+ * backward.  Returns -1 if `p` is invalid. */
+int64_t hydra_visible_pairs(const hydra_problem_t* p);
+
+/* Host-only view of the work plan, for tests.  which = 0: query-stationary items (forward
+ * and dQ), which = 1: key-stationary items (dK/dV).  Each item is 16 int32:
+ *   [0] first local row  [1] its global position  [2] rows in the tile  [3] n_ranges
+ *   [4+3r] first local row of range r on the other side, [5+3r] its global position,
+ *   [6+3r] rows in range r   (r < n_ranges <= HYDRA_MAX_SEGS)
+ * Items come in launch order (heaviest first).  Writes min(cap, n) items to `out` (may be
+ * NULL when cap = 0) and returns n, or a negative status. */
+int64_t hydra_plan_items(const hydra_problem_t* p, int32_t which, int32_t* out, int64_t cap);
+
+/* Tile sizes of the plan: rows per query-stationary tile, rows per key-stationary tile. */
+void hydra_tile_rows(int32_t* q_tile_rows, int32_t* kv_tile_rows);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HYDRA_ATTN_H */

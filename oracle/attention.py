@@ -85,7 +85,7 @@ def attn_fwd(q, k, v, cu_seqlens, q_segs, kv_segs, scale: Optional[float] = None
     LSE [H,Nq] float64 (natural log).  ``heads`` / ``q_rows`` restrict the work
     to a subset (other entries stay O=0, LSE=-inf); the full-size tests use them.
     """
-    Q, K, V = _f64(q), _f64(k), _f64(v)
+    Q, K, V = np.asarray(q), np.asarray(k), np.asarray(v)   # promoted to fp64 slice by slice
     nq, H, dqk = Q.shape
     tau = default_scale(dqk) if scale is None else float(scale)
     qpos, kpos = row_positions(q_segs), row_positions(kv_segs)
@@ -98,10 +98,11 @@ def attn_fwd(q, k, v, cu_seqlens, q_segs, kv_segs, scale: Optional[float] = None
             qi = qi[sel[qi]]
             if len(qi) == 0 or len(ki) == 0:
                 continue
+            Kd, Vd = _f64(K[ki, h, :]), _f64(V[ki, h, :])
             step = max(1, _SCORE_BLOCK // len(ki))
             for b in range(0, len(qi), step):
                 rows = qi[b:b + step]
-                s = tau * (Q[rows, h, :] @ K[ki, h, :].T)
+                s = tau * (_f64(Q[rows, h, :]) @ Kd.T)
                 vis = kpos[ki][None, :] <= qpos[rows][:, None]
                 s = np.where(vis, s, NEG_INF)
                 m = s.max(axis=1)
@@ -111,7 +112,7 @@ def attn_fwd(q, k, v, cu_seqlens, q_segs, kv_segs, scale: Optional[float] = None
                 l = e.sum(axis=1)
                 with np.errstate(divide="ignore"):
                     L[h, rows] = np.where(empty, NEG_INF, m_safe + np.log(l))
-                num = e @ V[ki, h, :]
+                num = e @ Vd
                 O[rows, h, :] = np.where(empty[:, None], 0.0, num / np.where(empty, 1.0, l)[:, None])
     return O, L
 
@@ -139,39 +140,46 @@ def lse_merge(o_a, lse_a, o_b, lse_b):
 
 
 def attn_bwd(q, k, v, o, lse, do, cu_seqlens, q_segs, kv_segs, scale: Optional[float] = None,
-             heads: Optional[Iterable[int]] = None):
+             heads: Optional[Iterable[int]] = None, q_rows: Optional[np.ndarray] = None):
     """Gradients of one ring step, given the final merged O and LSE of the rows.
 
     Returns dQ [Nq,H,dqk] (this step's contribution), dK [Nk,H,dqk], dV [Nk,H,dv].
+    ``q_rows`` restricts the queries taken into account: dQ is then computed for
+    those rows only, and dK/dV hold only their contributions (complete for a key
+    when every query that sees it is selected).
     """
-    Q, K, V, O, dO = _f64(q), _f64(k), _f64(v), _f64(o), _f64(do)
+    Q, K, V, O, dO = (np.asarray(x) for x in (q, k, v, o, do))   # fp64 slice by slice
     L = _f64(lse)
     nq, H, dqk = Q.shape
     tau = default_scale(dqk) if scale is None else float(scale)
     qpos, kpos = row_positions(q_segs), row_positions(kv_segs)
-    dQ = np.zeros_like(Q)
-    dK = np.zeros_like(K)
-    dV = np.zeros_like(V)
-    D = np.einsum("nhc,nhc->hn", dO, O)
+    dQ = np.zeros(Q.shape)
+    dK = np.zeros(K.shape)
+    dV = np.zeros(V.shape)
+    sel = np.ones(nq, bool) if q_rows is None else np.isin(np.arange(nq), q_rows)
     for h in (range(H) if heads is None else heads):
+        D = np.einsum("nc,nc->n", _f64(dO[:, h, :]), _f64(O[:, h, :]))
         for qi, ki in _groups(cu_seqlens, qpos, kpos):
+            qi = qi[sel[qi]]
             if len(qi) == 0 or len(ki) == 0:
                 continue
+            Kd, Vd = _f64(K[ki, h, :]), _f64(V[ki, h, :])
             step = max(1, _SCORE_BLOCK // len(ki))
             for b in range(0, len(qi), step):
                 rows = qi[b:b + step]
-                s = tau * (Q[rows, h, :] @ K[ki, h, :].T)
+                Qr, dOr = _f64(Q[rows, h, :]), _f64(dO[rows, h, :])
+                s = tau * (Qr @ Kd.T)
                 vis = kpos[ki][None, :] <= qpos[rows][:, None]
                 s = np.where(vis, s, NEG_INF)
                 lse_r = L[h, rows]
                 shift = np.where(np.isfinite(lse_r), lse_r, 0.0)
                 p = np.exp(s - shift[:, None])             # 0 on masked entries
                 p[~np.isfinite(lse_r)] = 0.0
-                dV[ki, h, :] += p.T @ dO[rows, h, :]
-                dp = dO[rows, h, :] @ V[ki, h, :].T
-                ds = p * (dp - D[h, rows][:, None])
-                dQ[rows, h, :] += tau * (ds @ K[ki, h, :])
-                dK[ki, h, :] += tau * (ds.T @ Q[rows, h, :])
+                dV[ki, h, :] += p.T @ dOr
+                dp = dOr @ Vd.T
+                ds = p * (dp - D[rows][:, None])
+                dQ[rows, h, :] += tau * (ds @ Kd)
+                dK[ki, h, :] += tau * (ds.T @ Qr)
     return dQ, dK, dV
 
 

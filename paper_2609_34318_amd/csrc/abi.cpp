@@ -1,0 +1,192 @@
+// The exported C ABI: validate on the host, plan, upload the plan, launch.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <vector>
+
+#include "hydra_attn.h"
+#include "kernels.h"
+#include "plan.h"
+
+namespace hydra {
+hipError_t launch_attn_fwd(const AttnArgs& a, uint16_t* o_bf16, hipStream_t stream);
+hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems,
+                           hipStream_t stream);
+hipError_t launch_lse_merge(int64_t n_rows, int H, float* o_acc, float* lse_acc, const float* o_part,
+                            const float* lse_part, uint16_t* o_bf16, hipStream_t stream);
+}  // namespace hydra
+
+using namespace hydra;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Non-null and 16-byte aligned when `needed`; HYDRA_OK otherwise.
+int check_ptr(const void* p, bool needed) {
+  if (!needed) return HYDRA_OK;
+  if (!p) return HYDRA_ERR_INVALID;
+  return aligned16(p) ? HYDRA_OK : HYDRA_ERR_ALIGN;
+}
+
+// Builds the host image of the workspace prefix (cu, query items, key items) and uploads it.
+int upload_plan(const Problem& pr, const WsLayout& w, bool with_kv_items, void* ws, hipStream_t stream,
+                std::vector<int32_t>* qitems, std::vector<int32_t>* kitems) {
+  plan_items(pr, 0, qitems);
+  if (with_kv_items) plan_items(pr, 1, kitems);
+  const size_t bytes = with_kv_items ? w.d_off : w.kitems_off;
+  std::vector<char> img(bytes, 0);
+  std::memcpy(img.data() + w.cu_off, pr.cu.data(), pr.cu.size() * sizeof(int32_t));
+  std::memcpy(img.data() + w.qitems_off, qitems->data(), qitems->size() * sizeof(int32_t));
+  if (with_kv_items) std::memcpy(img.data() + w.kitems_off, kitems->data(), kitems->size() * sizeof(int32_t));
+  // Pageable source: the runtime has consumed `img` when the call returns.
+  if (hipMemcpyAsync(ws, img.data(), bytes, hipMemcpyHostToDevice, stream) != hipSuccess) return HYDRA_ERR_HIP;
+  return HYDRA_OK;
+}
+
+AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
+  AttnArgs a{};
+  char* base = static_cast<char*>(ws);
+  a.cu = reinterpret_cast<const int*>(base + w.cu_off);
+  a.items = reinterpret_cast<const int*>(base + w.qitems_off);
+  a.Dvec = reinterpret_cast<float*>(base + w.d_off);
+  a.n_docs = int(pr.cu.size()) - 1;
+  a.H = pr.H;
+  a.nq = int(pr.nq);
+  a.nk = int(pr.nk);
+  a.scale = pr.scale;
+  return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t hydra_workspace_size(const hydra_problem_t* p) {
+  Problem pr;
+  if (check_problem(p, &pr) != HYDRA_OK) return 0;
+  return ws_layout(pr).total;
+}
+
+int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, float* o_part,
+                   float* lse_part, void* o_bf16, void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    Problem pr;
+    int rc = check_problem(p, &pr);
+    if (rc != HYDRA_OK) return rc;
+    if (pr.nq == 0) return HYDRA_OK;
+    const bool has_k = pr.nk > 0;
+    for (int c : {check_ptr(q, true), check_ptr(k, has_k), check_ptr(v, has_k), check_ptr(o_part, true),
+                  check_ptr(lse_part, true), o_bf16 ? check_ptr(o_bf16, true) : HYDRA_OK})
+      if (c != HYDRA_OK) return c;
+    const WsLayout w = ws_layout(pr);
+    if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    std::vector<int32_t> qitems, kitems;
+    rc = upload_plan(pr, w, false, workspace, s, &qitems, &kitems);
+    if (rc != HYDRA_OK) return rc;
+    AttnArgs a = base_args(pr, w, workspace);
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.out_o = o_part;
+    a.out_lse = lse_part;
+    a.n_items = int(w.n_qitems);
+    if (launch_attn_fwd(a, static_cast<uint16_t*>(o_bf16), s) != hipSuccess) return HYDRA_ERR_HIP;
+    return HYDRA_OK;
+  } catch (...) {
+    return HYDRA_ERR_INVALID;
+  }
+}
+
+int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, const void* o_final,
+                   const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc, float* dv_acc,
+                   void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    Problem pr;
+    int rc = check_problem(p, &pr);
+    if (rc != HYDRA_OK) return rc;
+    if (pr.nq == 0 || pr.nk == 0) return HYDRA_OK;
+    for (int c : {check_ptr(q, true), check_ptr(k, true), check_ptr(v, true), check_ptr(o_final, true),
+                  check_ptr(lse_final, true), check_ptr(d_o, true), check_ptr(dq_acc, true),
+                  check_ptr(dk_acc, true), check_ptr(dv_acc, true)})
+      if (c != HYDRA_OK) return c;
+    const WsLayout w = ws_layout(pr);
+    if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    std::vector<int32_t> qitems, kitems;
+    rc = upload_plan(pr, w, true, workspace, s, &qitems, &kitems);
+    if (rc != HYDRA_OK) return rc;
+    AttnArgs a = base_args(pr, w, workspace);
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.o = static_cast<const uint16_t*>(o_final);
+    a.dO = static_cast<const uint16_t*>(d_o);
+    a.lse = lse_final;
+    a.dq = dq_acc;
+    a.dk = dk_acc;
+    a.dv = dv_acc;
+    const int* kitems_dev = reinterpret_cast<const int*>(static_cast<char*>(workspace) + w.kitems_off);
+    if (launch_attn_bwd(a, int(w.n_qitems), int(w.n_kitems), kitems_dev, s) != hipSuccess) return HYDRA_ERR_HIP;
+    return HYDRA_OK;
+  } catch (...) {
+    return HYDRA_ERR_INVALID;
+  }
+}
+
+int hydra_lse_merge(int64_t n_rows, int32_t n_heads, int32_t d_v, float* o_acc, float* lse_acc,
+                    const float* o_part, const float* lse_part, void* o_out_bf16, void* stream) {
+  if (n_rows < 0 || n_heads <= 0 || n_heads > 4096) return HYDRA_ERR_INVALID;
+  if (d_v != kDv) return d_v <= 0 ? HYDRA_ERR_INVALID : HYDRA_ERR_UNSUPPORTED;
+  if (n_rows > (int64_t(1) << 30)) return HYDRA_ERR_INVALID;
+  if (n_rows == 0) return HYDRA_OK;
+  for (int c : {check_ptr(o_acc, true), check_ptr(lse_acc, true), check_ptr(o_part, true),
+                check_ptr(lse_part, true), o_out_bf16 ? check_ptr(o_out_bf16, true) : HYDRA_OK})
+    if (c != HYDRA_OK) return c;
+  if (launch_lse_merge(n_rows, n_heads, o_acc, lse_acc, o_part, lse_part, static_cast<uint16_t*>(o_out_bf16),
+                       static_cast<hipStream_t>(stream)) != hipSuccess)
+    return HYDRA_ERR_HIP;
+  return HYDRA_OK;
+}
+
+const char* hydra_strerror(int status) {
+  switch (status) {
+    case HYDRA_OK: return "ok";
+    case HYDRA_ERR_INVALID: return "invalid argument";
+    case HYDRA_ERR_UNSUPPORTED: return "unsupported problem (d_qk must be 192 and d_v 128)";
+    case HYDRA_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case HYDRA_ERR_WORKSPACE: return "workspace missing or too small";
+    case HYDRA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+int64_t hydra_visible_pairs(const hydra_problem_t* p) {
+  Problem pr;
+  if (check_problem(p, &pr) != HYDRA_OK) return -1;
+  return visible_pairs(pr);
+}
+
+int64_t hydra_plan_items(const hydra_problem_t* p, int32_t which, int32_t* out, int64_t cap) {
+  Problem pr;
+  int rc = check_problem(p, &pr);
+  if (rc != HYDRA_OK) return rc;
+  if (which != 0 && which != 1) return HYDRA_ERR_INVALID;
+  if (cap < 0 || (cap > 0 && !out)) return HYDRA_ERR_INVALID;
+  std::vector<int32_t> items;
+  plan_items(pr, which, &items);
+  const int64_t n = int64_t(items.size()) / kItemInts;
+  const int64_t k = n < cap ? n : cap;
+  if (k > 0) std::memcpy(out, items.data(), size_t(k) * kItemInts * sizeof(int32_t));
+  return n;
+}
+
+void hydra_tile_rows(int32_t* q_tile_rows, int32_t* kv_tile_rows) {
+  if (q_tile_rows) *q_tile_rows = kQTile;
+  if (kv_tile_rows) *kv_tile_rows = kKvTile;
+}
+
+}  // extern "C"

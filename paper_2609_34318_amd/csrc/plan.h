@@ -1,0 +1,43 @@
+// Host-side argument checks and work planning for one ring step (no HIP calls).
+#pragma once
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "hydra_attn.h"
+
+namespace hydra {
+
+constexpr int kDqk = 192;
+constexpr int kDv = 128;
+constexpr int kQTile = 128;    // query rows per query-stationary workgroup (4 waves x 32)
+constexpr int kKvTile = 128;   // key rows per key-stationary workgroup (4 waves x 32)
+constexpr int kItemInts = 16;  // int32 per work item
+
+// Checked and normalised view of a hydra_problem_t.
+struct Problem {
+  int H = 0;
+  float scale = 0.f;
+  std::vector<int32_t> cu;     // n_docs + 1 boundaries
+  hydra_chunk_t q{}, kv{};
+  int64_t nq = 0, nk = 0;
+};
+
+// Returns HYDRA_OK or an error status; fills `out` on success.
+int check_problem(const hydra_problem_t* p, Problem* out);
+
+// Work items (kItemInts each), heaviest first.  which = 0: query-stationary tiles of
+// kQTile rows with their visible key ranges; which = 1: key-stationary tiles of kKvTile
+// rows with their visible query ranges.
+void plan_items(const Problem& pr, int which, std::vector<int32_t>* items);
+
+int64_t visible_pairs(const Problem& pr);
+
+// Byte offsets of the workspace regions.
+struct WsLayout {
+  size_t cu_off, qitems_off, kitems_off, d_off, total;
+  int64_t n_qitems, n_kitems;
+};
+WsLayout ws_layout(const Problem& pr);
+
+}  // namespace hydra

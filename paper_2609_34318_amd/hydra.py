@@ -1,0 +1,180 @@
+"""ctypes binding of libhydra_attn.so: argument marshalling only.
+
+Every compute step runs in the library's HIP kernels; torch supplies device memory and
+the current stream.  If the library is missing this module raises on first use: there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhydra_attn.so")
+
+HYDRA_OK = 0
+MAX_SEGS = 4
+STATUS = {0: "ok", -1: "invalid", -2: "unsupported", -3: "align", -4: "workspace", -5: "hip"}
+
+
+class Chunk(ctypes.Structure):
+    _fields_ = [("n_segs", ctypes.c_int32),
+                ("start", ctypes.c_int32 * MAX_SEGS),
+                ("len", ctypes.c_int32 * MAX_SEGS)]
+
+
+class ProblemC(ctypes.Structure):
+    _fields_ = [("n_heads", ctypes.c_int32),
+                ("d_qk", ctypes.c_int32),
+                ("d_v", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float),
+                ("cu_seqlens", ctypes.POINTER(ctypes.c_int32)),
+                ("n_docs", ctypes.c_int32),
+                ("q", Chunk),
+                ("kv", Chunk)]
+
+
+class HydraError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what} failed: status {status} ({lib().hydra_strerror(status).decode()})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_34318_amd.build_lib`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER(ProblemC)
+        vp, f = ctypes.c_void_p, ctypes.POINTER(ctypes.c_float)
+        L.hydra_workspace_size.argtypes = [P]
+        L.hydra_workspace_size.restype = ctypes.c_size_t
+        L.hydra_attn_fwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.hydra_attn_fwd.restype = ctypes.c_int
+        L.hydra_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.hydra_attn_bwd.restype = ctypes.c_int
+        L.hydra_lse_merge.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp, vp]
+        L.hydra_lse_merge.restype = ctypes.c_int
+        L.hydra_strerror.argtypes = [ctypes.c_int]
+        L.hydra_strerror.restype = ctypes.c_char_p
+        L.hydra_visible_pairs.argtypes = [P]
+        L.hydra_visible_pairs.restype = ctypes.c_int64
+        L.hydra_plan_items.argtypes = [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.c_int64]
+        L.hydra_plan_items.restype = ctypes.c_int64
+        L.hydra_tile_rows.argtypes = [ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
+        L.hydra_tile_rows.restype = None
+        _lib = L
+    return _lib
+
+
+def _chunk(segs: Sequence[Tuple[int, int]]) -> Chunk:
+    segs = list(segs)
+    if len(segs) > MAX_SEGS:
+        raise ValueError(f"at most {MAX_SEGS} segments per chunk")
+    c = Chunk()
+    c.n_segs = len(segs)
+    for i, (s, n) in enumerate(segs):
+        c.start[i] = int(s)
+        c.len[i] = int(n)
+    return c
+
+
+class Problem:
+    """One ring step of one rank: head shard, documents, Q chunk and KV chunk."""
+
+    def __init__(self, cu_seqlens, n_heads: int, q_segs, kv_segs, softmax_scale: float = 0.0,
+                 d_qk: int = 192, d_v: int = 128):
+        self.cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
+        self.q_segs = [tuple(map(int, s)) for s in q_segs]
+        self.kv_segs = [tuple(map(int, s)) for s in kv_segs]
+        self.c = ProblemC()
+        self.c.n_heads = n_heads
+        self.c.d_qk = d_qk
+        self.c.d_v = d_v
+        self.c.softmax_scale = softmax_scale
+        self.c.cu_seqlens = self.cu.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+        self.c.n_docs = len(self.cu) - 1
+        self.c.q = _chunk(self.q_segs)
+        self.c.kv = _chunk(self.kv_segs)
+        self.n_heads = n_heads
+        self.nq = sum(n for _, n in self.q_segs)
+        self.nk = sum(n for _, n in self.kv_segs)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def workspace_size(p: Problem) -> int:
+    return int(lib().hydra_workspace_size(p.ref))
+
+
+def visible_pairs(p: Problem) -> int:
+    n = int(lib().hydra_visible_pairs(p.ref))
+    if n < 0:
+        raise HydraError(-1, "hydra_visible_pairs")
+    return n
+
+
+def plan_items(p: Problem, which: int) -> np.ndarray:
+    n = int(lib().hydra_plan_items(p.ref, which, None, 0))
+    if n < 0:
+        raise HydraError(n, "hydra_plan_items")
+    out = np.zeros((max(n, 1), 16), dtype=np.int32)
+    lib().hydra_plan_items(p.ref, which, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n)
+    return out[:n]
+
+
+def tile_rows() -> Tuple[int, int]:
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    lib().hydra_tile_rows(ctypes.byref(a), ctypes.byref(b))
+    return a.value, b.value
+
+
+# ------------------------------------------------------------------ device calls (torch tensors)
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check(rc: int, what: str):
+    if rc != HYDRA_OK:
+        raise HydraError(rc, what)
+
+
+def attn_fwd(p: Problem, q, k, v, o_part, lse_part, workspace, o_bf16=None, stream=None):
+    """Partial O (fp32) and LSE of one ring step; optional bf16 copy of O."""
+    _check(lib().hydra_attn_fwd(p.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o_part), _ptr(lse_part),
+                                _ptr(o_bf16), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                _stream(stream)), "hydra_attn_fwd")
+
+
+def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
+             stream=None):
+    """dQ/dK/dV of one ring step, accumulated (+=) into fp32 buffers."""
+    _check(lib().hydra_attn_bwd(p.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o_final_bf16), _ptr(lse_final),
+                                _ptr(d_o), _ptr(dq_acc), _ptr(dk_acc), _ptr(dv_acc), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(stream)),
+           "hydra_attn_bwd")
+
+
+def lse_merge(o_acc, lse_acc, o_part, lse_part, o_bf16=None, stream=None):
+    """(o_acc, lse_acc) <- exact merge with (o_part, lse_part), in place."""
+    n_rows, n_heads, d_v = o_acc.shape
+    _check(lib().hydra_lse_merge(n_rows, n_heads, d_v, _ptr(o_acc), _ptr(lse_acc), _ptr(o_part),
+                                 _ptr(lse_part), _ptr(o_bf16), _stream(stream)), "hydra_lse_merge")

@@ -20,8 +20,10 @@ imitates their stated profile (Sec. 2.2: most sequences short, a few very long).
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
 import math
+import os
 from typing import List, Sequence, Tuple
 
 import numpy as np
@@ -55,6 +57,14 @@ def _dist_scale(name: str, dist: str, d: int) -> float:
     raise ValueError(f"unknown distribution {dist!r}")
 
 
+def _block(t: int, b: int, seed: int, n_heads: int, d: int, scale: np.float32) -> np.ndarray:
+    g = np.random.default_rng([seed, t, b])
+    blk = g.standard_normal((BLOCK_ROWS, n_heads, d), dtype=np.float32)
+    if scale != 1:
+        blk *= scale
+    return bf16_round_bits(blk)
+
+
 def rows(name: str, segments: Segments, n_heads: int, d: int, seed: int = 0,
          dist: str = "paper") -> np.ndarray:
     """bf16 bit patterns, shape [sum(len), n_heads, d], rows in segment order."""
@@ -62,23 +72,39 @@ def rows(name: str, segments: Segments, n_heads: int, d: int, seed: int = 0,
     scale = np.float32(_dist_scale(name, dist, d))
     total = sum(n for _, n in segments)
     out = np.empty((total, n_heads, d), dtype=np.uint16)
+    pieces = []   # (out offset, block, lo, hi)
     o = 0
-    cache = {}
     for start, n in segments:
-        p = start
-        end = start + n
+        p, end = start, start + n
         while p < end:
             b = p // BLOCK_ROWS
-            if b not in cache:
-                g = np.random.default_rng([seed, t, b])
-                blk = g.standard_normal((BLOCK_ROWS, n_heads, d), dtype=np.float32)
-                cache = {b: bf16_round_bits(blk * scale)}
             lo = p - b * BLOCK_ROWS
             hi = min(end, (b + 1) * BLOCK_ROWS) - b * BLOCK_ROWS
-            out[o:o + hi - lo] = cache[b][lo:hi]
+            pieces.append((o, b, lo, hi))
             o += hi - lo
             p += hi - lo
+    blocks = sorted({b for _, b, _, _ in pieces})
+
+    def fill(b):
+        blk = _block(t, b, seed, n_heads, d, scale)
+        for off, bb, lo, hi in pieces:
+            if bb == b:
+                out[off:off + hi - lo] = blk[lo:hi]
+
+    if len(blocks) <= 1:
+        for b in blocks:
+            fill(b)
+    else:
+        with cf.ThreadPoolExecutor(max_workers=min(len(blocks), _threads())) as ex:
+            list(ex.map(fill, blocks))
     return out
+
+
+def _threads() -> int:
+    try:
+        return max(1, min(16, len(os.sched_getaffinity(0))))
+    except AttributeError:
+        return max(1, min(16, os.cpu_count() or 1))
 
 
 # ---------------------------------------------------------------- document mixes

@@ -1,0 +1,342 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Small and medium problems are compared element by element; the full-size workloads
+(32K packed microbatch, 256K ring steps, 128K zigzag share) on sampled rows the oracle
+computes one by one, on uniform-logit closed forms over every element, and on
+identities that hold at any size."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import attention as A
+from paper_2609_34318_amd import hydra, inputs, ring
+
+from gpu_util import (TOL_GRAD, TOL_LSE, TOL_O, assert_grad_close, assert_lse_close, assert_o_close,
+                      dev_bf16, f32, rel_l2)
+
+pytestmark = pytest.mark.gpu
+
+D_QK, D_V = 192, 128
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    hydra.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0):
+    """Forward (and backward if dO given) of a share; returns numpy results."""
+    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale)
+    q = dev_bf16(q_bits)
+    kv = [(dev_bf16(k), dev_bf16(v)) for k, v in kv_bits]
+    o, lse, o16 = ring.forward(sh, q, kv)
+    res = {"o": o.cpu().numpy(), "lse": lse.cpu().numpy(), "o16": o16.float().cpu().numpy()}
+    if do_bits is not None:
+        d_o = dev_bf16(do_bits)
+        dq = torch.zeros((sh.nq, H, D_QK), dtype=torch.float32, device="cuda")
+        dkv = [(torch.zeros((k.shape[0], H, D_QK), dtype=torch.float32, device="cuda"),
+                torch.zeros((k.shape[0], H, D_V), dtype=torch.float32, device="cuda")) for k, _ in kv]
+        ring.backward(sh, q, kv, d_o, dq, dkv)
+        res["dq"] = dq.cpu().numpy()
+        res["dkv"] = [(a.cpu().numpy(), b.cpu().numpy()) for a, b in dkv]
+    torch.cuda.synchronize()
+    return res
+
+
+def _gen(cu, H, q_segs, steps, dist="paper", seed=0, bwd=False):
+    q = inputs.rows("q", q_segs, H, D_QK, seed, dist)
+    kv = [(inputs.rows("k", s, H, D_QK, seed, dist), inputs.rows("v", s, H, D_V, seed, dist)) for s in steps]
+    do = inputs.rows("do", q_segs, H, D_V, seed, dist) if bwd else None
+    return q, kv, do
+
+
+def _union(steps):
+    return [seg for s in steps for seg in s]
+
+
+def _oracle_share(cu, q_segs, steps, q, kv, do=None, scale=None):
+    """Unsplit forward over the union of the steps' chunks, then per-step backward."""
+    union = _union(steps)
+    k_all = np.concatenate([f32(k) for k, _ in kv]) if kv else np.zeros((0, q.shape[1], D_QK), np.float32)
+    v_all = np.concatenate([f32(v) for _, v in kv]) if kv else np.zeros((0, q.shape[1], D_V), np.float32)
+    O, L = oracle.attn_fwd(f32(q), k_all, v_all, cu, q_segs, union, scale=scale)
+    out = {"o": O, "lse": L}
+    if do is not None:
+        out["dq"] = np.zeros(q.shape)
+        out["dkv"] = []
+        for s, (k, v) in zip(steps, kv):
+            dq, dk, dv = oracle.attn_bwd(f32(q), f32(k), f32(v), O, L, f32(do), cu, q_segs, s, scale=scale)
+            out["dq"] += dq
+            out["dkv"].append((dk, dv))
+    return out
+
+
+def _check_fwd(res, ref):
+    assert_lse_close(res["lse"], ref["lse"])
+    assert_o_close(res["o"], ref["o"])
+    assert_o_close(res["o16"], ref["o"], what="O bf16")
+
+
+def _check_bwd(res, ref):
+    assert_grad_close(res["dq"], ref["dq"], what="dQ")
+    for i, ((dk, dv), (rk, rv)) in enumerate(zip(res["dkv"], ref["dkv"])):
+        if np.linalg.norm(rk) > 0:
+            assert_grad_close(dk, rk, what=f"dK step {i}")
+            assert_grad_close(dv, rv, what=f"dV step {i}")
+        else:
+            assert np.abs(dk).max() == 0 and np.abs(dv).max() == 0
+
+
+# ----------------------------------------------------------------- small: element by element
+
+def test_tiny_two_step_forward_partials_and_merge():
+    w = inputs.WORKLOADS["tiny_2step"]
+    cu, H = list(w.cu_seqlens), w.n_heads
+    steps = [list(s) for s in w.kv_steps]
+    q, kv, _ = _gen(cu, H, list(w.q_segs), steps)
+    # each partial on its own
+    for s, (k, v) in zip(steps, kv):
+        res = _run_share(cu, H, list(w.q_segs), [s], q, [(k, v)])
+        O, L = oracle.attn_fwd(f32(q), f32(k), f32(v), cu, list(w.q_segs), s)
+        _check_fwd(res, {"o": O, "lse": L})
+    # step B (keys 256..511) leaves rows 0..255 empty: the -inf path
+    res = _run_share(cu, H, list(w.q_segs), steps, q, kv)
+    _check_fwd(res, _oracle_share(cu, list(w.q_segs), steps, q, kv))
+
+
+MEDIUM = {
+    # documents with an empty one and single-token ones; lengths not multiples of any tile
+    "contiguous_1step": ([0, 300, 300, 301, 1000, 1050, 1333], [(0, 1333)], [[(0, 1333)]]),
+    "ragged_3step": ([0, 300, 300, 301, 1000, 1050, 1333], [(0, 1333)],
+                     [[(0, 77)], [(77, 500), (1300, 33)], [(577, 723)]]),
+    "zigzag_2step": ([0, 1024], list(inputs.zigzag_segments(1024, 2, 0)),
+                     [list(inputs.zigzag_segments(1024, 2, 0)), list(inputs.zigzag_segments(1024, 2, 1))]),
+    "q_subset_4seg": ([0, 200, 900, 1400], [(50, 100), (850, 200), (1300, 37), (0, 1)],
+                      [[(0, 450)], [(450, 950)]]),
+}
+
+
+@pytest.mark.parametrize("dist", ["paper", "sharp", "spiky"])
+@pytest.mark.parametrize("layout", list(MEDIUM))
+def test_medium_forward_backward(layout, dist):
+    cu, q_segs, steps = MEDIUM[layout]
+    H = 3
+    q, kv, do = _gen(cu, H, q_segs, steps, dist=dist, seed=1, bwd=True)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do)
+    ref = _oracle_share(cu, q_segs, steps, q, kv, do)
+    _check_fwd(res, ref)
+    _check_bwd(res, ref)
+
+
+def test_nondefault_scale():
+    cu, q_segs, steps = MEDIUM["ragged_3step"]
+    q, kv, do = _gen(cu, 2, q_segs, steps, dist="sharp", seed=2, bwd=True)
+    res = _run_share(cu, 2, q_segs, steps, q, kv, do, scale=0.11)
+    ref = _oracle_share(cu, q_segs, steps, q, kv, do, scale=0.11)
+    _check_fwd(res, ref)
+    _check_bwd(res, ref)
+
+
+def test_constant_v_gives_constant_and_single_key_rows():
+    cu = [0, 64, 192, 512]
+    segs = [(0, 512)]
+    q, kv, _ = _gen(cu, 4, segs, [segs], dist="sharp")
+    k, v = kv[0]
+    half = np.full(v.shape, inputs.bf16_round_bits(np.float32([0.5]))[0], dtype=np.uint16)
+    res = _run_share(cu, 4, segs, [segs], q, [(k, half)])
+    assert np.abs(res["o"] - 0.5).max() <= 2e-3
+    res = _run_share(cu, 4, segs, [segs], q, [(k, v)])
+    tau = 1 / math.sqrt(D_QK)
+    for r in (0, 64, 192):
+        np.testing.assert_allclose(res["o"][r], f32(v)[r], atol=1e-6)
+        s_rr = tau * np.einsum("hc,hc->h", f32(q)[r].astype(np.float64), f32(k)[r].astype(np.float64))
+        np.testing.assert_allclose(res["lse"][:, r], s_rr, atol=TOL_LSE)
+
+
+def test_empty_kv_chunk_and_fully_masked_step():
+    cu = [0, 700]
+    q_segs = [(300, 200)]
+    q, _, _ = _gen(cu, 2, q_segs, [])
+    for steps in ([[]], [[(600, 100)]], [[(0, 0), (650, 0)]]):
+        kv = [(inputs.rows("k", s, 2, D_QK), inputs.rows("v", s, 2, D_V)) for s in steps]
+        res = _run_share(cu, 2, q_segs, steps, q, kv)
+        assert np.isneginf(res["lse"]).all()
+        assert (res["o"] == 0).all()
+
+
+def test_every_output_written_and_deterministic():
+    cu, q_segs, steps = MEDIUM["ragged_3step"]
+    H = 2
+    q, kv, do = _gen(cu, H, q_segs, steps, dist="spiky", seed=3, bwd=True)
+    p = hydra.Problem(cu, H, q_segs, steps[1])
+    ws = torch.empty(hydra.workspace_size(p), dtype=torch.uint8, device="cuda")
+    qd = dev_bf16(q)
+    kd, vd = dev_bf16(kv[1][0]), dev_bf16(kv[1][1])
+    outs = []
+    for _ in range(2):
+        o = torch.full((p.nq, H, D_V), float("nan"), device="cuda")
+        lse = torch.full((H, p.nq), float("nan"), device="cuda")
+        hydra.attn_fwd(p, qd, kd, vd, o, lse, ws)
+        torch.cuda.synchronize()
+        assert not torch.isnan(o).any() and not torch.isnan(lse).any()
+        outs.append((o.clone(), lse.clone()))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    grads = []
+    for _ in range(2):
+        res = _run_share(cu, H, q_segs, steps, q, kv, do)
+        grads.append(res)
+    assert np.array_equal(grads[0]["dq"], grads[1]["dq"])
+    for (a, b), (c, d) in zip(grads[0]["dkv"], grads[1]["dkv"]):
+        assert np.array_equal(a, c) and np.array_equal(b, d)
+
+
+def test_gradient_canaries_untouched():
+    """dK/dV rows outside the KV chunk's rows are never written (guard bands)."""
+    cu = [0, 500]
+    segs = [(0, 500)]
+    H = 2
+    q, kv, do = _gen(cu, H, segs, [segs], bwd=True)
+    p = hydra.Problem(cu, H, segs, segs)
+    sh = ring.make_share(cu, H, segs, [segs])
+    qd, kd, vd, dod = dev_bf16(q), dev_bf16(kv[0][0]), dev_bf16(kv[0][1]), dev_bf16(do)
+    ring.forward(sh, qd, [(kd, vd)])
+    guard = 64
+    dq = torch.full((500 + 2 * guard, H, D_QK), 7.0, device="cuda")
+    dk = torch.full((500 + 2 * guard, H, D_QK), 7.0, device="cuda")
+    dv = torch.full((500 + 2 * guard, H, D_V), 7.0, device="cuda")
+    hydra.attn_bwd(p, qd, kd, vd, sh.o_bf16, sh.lse_acc, dod, dq[guard:-guard], dk[guard:-guard],
+                   dv[guard:-guard], sh.workspace)
+    torch.cuda.synchronize()
+    for t in (dq, dk, dv):
+        assert (t[:guard] == 7.0).all() and (t[-guard:] == 7.0).all()
+
+
+# ----------------------------------------------------------------- full-size workloads
+
+def _sample_rows(n, extra, count, seed):
+    rng = np.random.default_rng(seed)
+    r = set(int(x) for x in rng.choice(n, size=min(count, n), replace=False))
+    r.update(int(x) for x in extra if 0 <= x < n)
+    return np.array(sorted(r))
+
+
+def test_packed32k_forward_sampled_rows():
+    w = inputs.WORKLOADS["packed32k_fwd"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, _ = _gen(cu, H, q_segs, steps)
+    res = _run_share(cu, H, q_segs, steps, q, kv)
+    assert np.isfinite(res["o"]).all() and np.isfinite(res["lse"]).all()
+    edges = [c + d for c in cu for d in (-1, 0, 1)] + [127, 128, 129, 16383]
+    rows = _sample_rows(32768, edges, 160, 0)
+    heads = [0, 5, 15]
+    O, L = oracle.attn_fwd(f32(q)[:, heads], f32(kv[0][0])[:, heads], f32(kv[0][1])[:, heads], cu, q_segs,
+                           steps[0], q_rows=rows)
+    assert_o_close(res["o"][rows][:, heads], O[rows])
+    assert_o_close(res["o16"][rows][:, heads], O[rows], what="O bf16")
+    assert_lse_close(res["lse"][heads][:, rows], L[:, rows])
+
+
+def test_ring256k_three_steps_uniform_closed_form_and_sampled_rows():
+    w = inputs.WORKLOADS["ring256k_3step"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, _ = _gen(cu, H, q_segs, steps)
+    # (1) Q = 0: every logit is 0, so O is the mean of the visible V and LSE = ln(count), all rows
+    zq = np.zeros_like(q)
+    res = _run_share(cu, H, q_segs, steps, zq, kv)
+    v_all = np.concatenate([f32(v) for _, v in kv])
+    Uo, UL, n = oracle.uniform_fwd(v_all, cu, q_segs, _union(steps))
+    assert_lse_close(res["lse"], UL)
+    assert_o_close(res["o"], Uo)
+    # (2) real inputs, sampled rows of all steps merged; step (c) alone is fully masked
+    res = _run_share(cu, H, q_segs, steps, q, kv)
+    rows = _sample_rows(32768, [0, 1, 127, 128, 32767], 48, 1)
+    heads = [3, 12]
+    k_all = np.concatenate([f32(k)[:, heads] for k, _ in kv])
+    O, L = oracle.attn_fwd(f32(q)[:, heads], k_all, v_all[:, heads], cu, q_segs, _union(steps), q_rows=rows)
+    assert_o_close(res["o"][rows][:, heads], O[rows])
+    assert_lse_close(res["lse"][heads][:, rows], L[:, rows])
+    res_c = _run_share(cu, H, q_segs, [steps[2]], q, [kv[2]])
+    assert np.isneginf(res_c["lse"]).all() and (res_c["o"] == 0).all()
+
+
+def test_packed32k_backward_full_heads():
+    w = inputs.WORKLOADS["packed32k_fwdbwd"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do)
+    heads = [1, 9]
+    sub = lambda x: f32(x)[:, heads]
+    O, L = oracle.attn_fwd(sub(q), sub(kv[0][0]), sub(kv[0][1]), cu, q_segs, steps[0])
+    dq, dk, dv = oracle.attn_bwd(sub(q), sub(kv[0][0]), sub(kv[0][1]), O, L, sub(do), cu, q_segs, steps[0])
+    assert_o_close(res["o"][:, heads], O)
+    assert_lse_close(res["lse"][heads], L)
+    assert_grad_close(res["dq"][:, heads], dq, what="dQ")
+    assert_grad_close(res["dkv"][0][0][:, heads], dk, what="dK")
+    assert_grad_close(res["dkv"][0][1][:, heads], dv, what="dV")
+    # identities over every head: per document, sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i
+    # (exact in the oracle; here the per-row errors, within tolerance, add up randomly)
+    gdk, gdv = (x.astype(np.float64) for x in res["dkv"][0])
+    dof = f32(do).astype(np.float64)
+    for a, b in zip(cu[:-1], cu[1:]):
+        for h in range(H):
+            assert np.linalg.norm(gdk[a:b, h].sum(0)) <= 0.05 * np.linalg.norm(gdk[a:b, h]) + 1e-6
+            err = np.linalg.norm(gdv[a:b, h].sum(0) - dof[a:b, h].sum(0))
+            assert err <= 0.05 * np.linalg.norm(gdv[a:b, h]) + 1e-6
+
+
+def test_zigzag256k_share_sampled_rows_and_tail_keys():
+    w = inputs.WORKLOADS["zigzag256k_share"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do)
+    heads = [2, 13]
+    nq = 131072
+    # query rows: head quarter, tail quarter, its last rows (which see the tail keys below)
+    tail_q = np.arange(nq - 64, nq)
+    rows = np.unique(np.concatenate([_sample_rows(nq, [0, 65535, 65536], 24, 2), tail_q]))
+    union = [(0, 262144)]
+    k_all = f32(inputs.rows("k", union, H, D_QK))[:, heads]
+    v_all = f32(inputs.rows("v", union, H, D_V))[:, heads]
+    qh, doh = f32(q)[:, heads], f32(do)[:, heads]
+    O, L = oracle.attn_fwd(qh, k_all, v_all, cu, q_segs, union, q_rows=rows)
+    assert_o_close(res["o"][rows][:, heads], O[rows])
+    assert_lse_close(res["lse"][heads][:, rows], L[:, rows])
+    # dQ of the sampled rows, summed over both steps, and dK/dV of the last 64 keys of step 0
+    # (positions 262080..262143, seen only by the 64 tail queries)
+    dq_ref = np.zeros((nq, 2, D_QK))
+    for si, s in enumerate(steps):
+        kk = f32(kv[si][0])[:, heads]
+        vv = f32(kv[si][1])[:, heads]
+        dq, dk, dv = oracle.attn_bwd(qh, kk, vv, O, L, doh, cu, q_segs, s, q_rows=rows)
+        dq_ref += dq
+        if si == 0:
+            tail_k = np.arange(nq - 64, nq)
+            assert_grad_close(res["dkv"][0][0][tail_k][:, heads], dk[tail_k], what="dK tail")
+            assert_grad_close(res["dkv"][0][1][tail_k][:, heads], dv[tail_k], what="dV tail")
+    assert_grad_close(res["dq"][rows][:, heads], dq_ref[rows], what="dQ rows")
+
+
+def test_zigzag256k_uniform_closed_form_backward():
+    """K = 0: softmax is uniform; O, LSE over every row and dK/dV of sampled keys of the
+    peer chunk (each seen by 64K queries) have closed forms."""
+    w = inputs.WORKLOADS["zigzag256k_share"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), 2, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
+    kv0 = [(np.zeros_like(k), v) for k, v in kv]
+    res = _run_share(cu, H, q_segs, steps, q, kv0, do)
+    v_all = np.concatenate([f32(v) for _, v in kv])
+    Uo, UL, n = oracle.uniform_fwd(v_all, cu, q_segs, _union(steps))
+    assert_lse_close(res["lse"], UL)
+    assert_o_close(res["o"], Uo)
+    assert np.abs(res["dq"]).max() == 0.0
+    keys = np.array([0, 1, 4095, 65535, 65536, 100000, 131071])
+    dk, dv = oracle.uniform_bwd_k0(f32(q), f32(kv[1][1]), Uo, f32(do), n, cu, q_segs, steps[1], keys)
+    assert_grad_close(res["dkv"][1][0][keys], dk, what="dK uniform")
+    assert_grad_close(res["dkv"][1][1][keys], dv, what="dV uniform")

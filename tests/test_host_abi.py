@@ -1,0 +1,154 @@
+"""CPU tests of the C library: it loads, exports every declared symbol, validates its
+arguments, and its work plan covers exactly the visible (query, key) pairs."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import attention as A
+from paper_2609_34318_amd import hydra, inputs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    if not os.path.exists(hydra.LIB_PATH):
+        from paper_2609_34318_amd import build_lib
+        build_lib.build()
+    return hydra.lib()
+
+
+def test_library_exports_every_declared_function():
+    text = open(os.path.join(ROOT, "include", "hydra_attn.h")).read()
+    names = set(re.findall(r"\b(hydra_[a-z0-9_]+)\s*\(", text))
+    assert {"hydra_attn_fwd", "hydra_attn_bwd", "hydra_lse_merge", "hydra_workspace_size"} <= names
+    L = hydra.lib()
+    for n in sorted(names):
+        assert hasattr(L, n), f"{n} not exported"
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4, -5, 7):
+        assert isinstance(hydra.lib().hydra_strerror(code), bytes)
+
+
+def _problem(cu, H, q, kv, **kw):
+    return hydra.Problem(cu, H, q, kv, **kw)
+
+
+@pytest.mark.parametrize("case", [
+    dict(cu=[0, 100], H=0, q=[(0, 10)], kv=[(0, 10)]),            # no heads
+    dict(cu=[1, 100], H=2, q=[(0, 10)], kv=[(0, 10)]),            # cu[0] != 0
+    dict(cu=[0, 100, 50], H=2, q=[(0, 10)], kv=[(0, 10)]),        # not monotone
+    dict(cu=[0, 100], H=2, q=[(95, 10)], kv=[(0, 10)]),           # segment past the window
+    dict(cu=[0, 100], H=2, q=[(0, 10)], kv=[(-1, 5)]),            # negative start
+    dict(cu=[0, 100], H=2, q=[(0, 10)], kv=[(0, -5)]),            # negative length
+])
+def test_invalid_problems_rejected_on_host(case):
+    p = _problem(case["cu"], case["H"], case["q"], case["kv"])
+    assert hydra.workspace_size(p) == 0
+    assert hydra.lib().hydra_visible_pairs(p.ref) == -1
+    # the compute calls reject before touching the GPU (null pointers would fault otherwise)
+    L = hydra.lib()
+    assert L.hydra_attn_fwd(p.ref, None, None, None, None, None, None, None, 0, None) == -1
+    assert L.hydra_attn_bwd(p.ref, *([None] * 10), 0, None) == -1
+
+
+def test_unsupported_dims_and_bad_pointers():
+    L = hydra.lib()
+    p = _problem([0, 64], 2, [(0, 64)], [(0, 64)], d_qk=128)
+    assert L.hydra_attn_fwd(p.ref, None, None, None, None, None, None, None, 0, None) == -2
+    p = _problem([0, 64], 2, [(0, 64)], [(0, 64)])
+    ws = hydra.workspace_size(p)
+    assert ws > 0
+    # misaligned device pointers: rejected with HYDRA_ERR_ALIGN before any HIP call
+    assert L.hydra_attn_fwd(p.ref, 8, 16, 16, 16, 16, None, 16, ws, None) == -3
+    # workspace too small / missing
+    assert L.hydra_attn_fwd(p.ref, 16, 16, 16, 16, 16, None, 16, ws - 1, None) == -4
+    assert L.hydra_attn_fwd(p.ref, 16, 16, 16, 16, 16, None, None, ws, None) == -4
+    # merge argument checks
+    assert L.hydra_lse_merge(10, 2, 64, 16, 16, 16, 16, None, None) == -2
+    assert L.hydra_lse_merge(-1, 2, 128, 16, 16, 16, 16, None, None) == -1
+    assert L.hydra_lse_merge(10, 2, 128, 16, 16, 8, 16, None, None) == -3
+    assert L.hydra_lse_merge(0, 2, 128, None, None, None, None, None, None) == 0
+
+
+def test_zero_rows_is_noop():
+    L = hydra.lib()
+    p = _problem([0, 64], 2, [], [(0, 64)])
+    assert L.hydra_attn_fwd(p.ref, None, None, None, None, None, None, None, 0, None) == 0
+    p = _problem([0, 64], 2, [(0, 64)], [])
+    assert L.hydra_attn_bwd(p.ref, *([None] * 10), 0, None) == 0
+
+
+def _random_problem(rng):
+    n_docs = int(rng.integers(1, 8))
+    lens = rng.integers(0, 400, size=n_docs)
+    lens[int(rng.integers(0, n_docs))] += 1
+    cu = inputs.cu_from_lengths(lens)
+    total = int(cu[-1])
+
+    def chunk():
+        segs = []
+        for _ in range(int(rng.integers(0, 5))):
+            a = int(rng.integers(0, total + 1))
+            b = int(rng.integers(a, total + 1))
+            segs.append((a, b - a))
+        return segs
+
+    return cu, chunk(), chunk()
+
+
+def _covered(items, nq, nk, which):
+    """Count how often each (query row, key row) pair is visited by the plan."""
+    cov = np.zeros((nq, nk), dtype=np.int32)
+    for it in items:
+        r0, n, nr = it[0], it[2], it[3]
+        for r in range(nr):
+            o0, on = it[4 + 3 * r], it[6 + 3 * r]
+            if which == 0:
+                cov[r0:r0 + n, o0:o0 + on] += 1
+            else:
+                cov[o0:o0 + on, r0:r0 + n] += 1
+    return cov
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_plan_covers_exactly_the_visible_pairs(seed):
+    rng = np.random.default_rng(seed)
+    cu, q_segs, kv_segs = _random_problem(rng)
+    p = _problem(cu, 3, q_segs, kv_segs)
+    qpos, kpos = A.row_positions(q_segs), A.row_positions(kv_segs)
+    qd, kd = A.doc_of(cu, qpos), A.doc_of(cu, kpos)
+    vis = (qd[:, None] == kd[None, :]) & (kpos[None, :] <= qpos[:, None])
+    assert hydra.visible_pairs(p) == int(vis.sum()) == A.visible_pairs_bruteforce(cu, q_segs, kv_segs)
+    bq, bk = hydra.tile_rows()
+    for which, rows_per_tile in ((0, bq), (1, bk)):
+        items = hydra.plan_items(p, which)
+        cov = _covered(items, len(qpos), len(kpos), which)
+        assert (cov <= 1).all(), "a pair is visited twice"
+        assert (cov[vis] == 1).all(), "a visible pair is never visited"
+        own = qpos if which == 0 else kpos
+        own_rows = sorted(r for it in items for r in range(it[0], it[0] + it[2]))
+        assert own_rows == list(range(len(own))), "tiles must cover every own row once"
+        for it in items:
+            assert 1 <= it[2] <= rows_per_tile
+            seg_pos = own[it[0]:it[0] + it[2]]
+            assert seg_pos[0] == it[1] and (np.diff(seg_pos) == 1).all(), "tile rows must be consecutive"
+        cost = [sum(it[6 + 3 * r] for r in range(it[3])) for it in items]
+        assert cost == sorted(cost, reverse=True), "heaviest tiles first"
+
+
+def test_visible_pairs_of_the_workloads():
+    expect = {"tiny_2step": [28800, 32896],
+              "packed32k_fwd": [144931409],
+              "ring256k_3step": [536887296, 1073741824, 0],
+              "zigzag256k_share": [8590000128, 8589934592]}
+    for name, counts in expect.items():
+        w = inputs.WORKLOADS[name]
+        got = [hydra.visible_pairs(hydra.Problem(w.cu_seqlens, w.n_heads, w.q_segs, s)) for s in w.kv_steps]
+        assert got == counts, name
+    # the packed microbatch: sum of s(s+1)/2 over its documents
+    assert 144931409 == sum(s * (s + 1) // 2 for s in inputs.PACKED32K_DOCS)

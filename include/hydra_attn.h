@@ -133,6 +133,23 @@ int64_t hydra_plan_items(const hydra_problem_t* p, int32_t which, int32_t* out, 
 /* Tile sizes of the plan: rows per query-stationary tile, rows per key-stationary tile. */
 void hydra_tile_rows(int32_t* q_tile_rows, int32_t* kv_tile_rows);
 
+/* Per-kernel timing (a tracing aid for benchmarks; off by default).  While recording, every
+ * kernel this library launches is bracketed by two hipEvents on its launch stream.
+ * hydra_profile_start() clears earlier records and starts recording.
+ * hydra_profile_stop() waits for the recorded events, stops recording, writes up to `cap`
+ * per-kernel summaries to `out` and returns the number of distinct kernels (or a negative
+ * status).  Names: "attn_fwd", "bwd_pre", "bwd_dq", "bwd_dkdv", "lse_merge". */
+typedef struct {
+  char    name[32];
+  int64_t launches;
+  double  total_ms;
+  double  min_ms;
+  double  max_ms;
+} hydra_kernel_stat_t;
+
+int hydra_profile_start(void);
+int hydra_profile_stop(hydra_kernel_stat_t* out, int32_t cap);
+
 #ifdef __cplusplus
 }
 #endif

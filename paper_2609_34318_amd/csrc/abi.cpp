@@ -1,12 +1,17 @@
 // The exported C ABI: validate on the host, plan, upload the plan, launch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
 #include <vector>
 
 #include "hydra_attn.h"
 #include "kernels.h"
 #include "plan.h"
+#include "prof.h"
 
 namespace hydra {
 hipError_t launch_attn_fwd(const AttnArgs& a, uint16_t* o_bf16, hipStream_t stream);
@@ -17,6 +22,49 @@ hipError_t launch_lse_merge(int64_t n_rows, int H, float* o_acc, float* lse_acc,
 }  // namespace hydra
 
 using namespace hydra;
+
+// ------------------------------------------------------------------ kernel timing
+namespace {
+struct ProfRec {
+  const char* name;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+}  // namespace
+
+namespace hydra {
+int prof_begin(const char* kernel, hipStream_t stream) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  if (!g_prof_on) return -1;
+  ProfRec r{kernel, nullptr, nullptr};
+  if (hipEventCreate(&r.start) != hipSuccess) return -1;
+  if (hipEventCreate(&r.stop) != hipSuccess) {
+    (void)hipEventDestroy(r.start);
+    return -1;
+  }
+  (void)hipEventRecord(r.start, stream);
+  g_prof.push_back(r);
+  return int(g_prof.size()) - 1;
+}
+void prof_end(int token, hipStream_t stream) {
+  if (token < 0) return;
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  if (token < int(g_prof.size())) (void)hipEventRecord(g_prof[token].stop, stream);
+}
+}  // namespace hydra
+
+namespace {
+void prof_clear_locked() {
+  for (ProfRec& r : g_prof) {
+    if (r.stop) (void)hipEventSynchronize(r.stop);
+    (void)hipEventDestroy(r.start);
+    (void)hipEventDestroy(r.stop);
+  }
+  g_prof.clear();
+}
+}  // namespace
 
 namespace {
 
@@ -181,6 +229,47 @@ int64_t hydra_plan_items(const hydra_problem_t* p, int32_t which, int32_t* out, 
   const int64_t n = int64_t(items.size()) / kItemInts;
   const int64_t k = n < cap ? n : cap;
   if (k > 0) std::memcpy(out, items.data(), size_t(k) * kItemInts * sizeof(int32_t));
+  return n;
+}
+
+int hydra_profile_start(void) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  prof_clear_locked();
+  g_prof_on = true;
+  return HYDRA_OK;
+}
+
+int hydra_profile_stop(hydra_kernel_stat_t* out, int32_t cap) {
+  std::lock_guard<std::mutex> lock(g_prof_mu);
+  g_prof_on = false;
+  if (cap < 0 || (cap > 0 && !out)) return HYDRA_ERR_INVALID;
+  std::map<std::string, hydra_kernel_stat_t> agg;
+  int status = HYDRA_OK;
+  for (ProfRec& r : g_prof) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.stop) != hipSuccess || hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+      status = HYDRA_ERR_HIP;
+      continue;
+    }
+    hydra_kernel_stat_t& k = agg[r.name];
+    if (k.launches == 0) {
+      std::memset(&k, 0, sizeof(k));
+      std::strncpy(k.name, r.name, sizeof(k.name) - 1);
+      k.min_ms = ms;
+      k.max_ms = ms;
+    }
+    k.launches += 1;
+    k.total_ms += ms;
+    k.min_ms = std::min<double>(k.min_ms, ms);
+    k.max_ms = std::max<double>(k.max_ms, ms);
+  }
+  prof_clear_locked();
+  if (status != HYDRA_OK) return status;
+  int n = 0;
+  for (auto& kv : agg) {
+    if (n < cap) out[n] = kv.second;
+    ++n;
+  }
   return n;
 }
 

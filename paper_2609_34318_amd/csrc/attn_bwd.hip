@@ -8,6 +8,7 @@
 // Splitting dQ from dK/dV recomputes S and dP once more but needs no atomics and is
 // deterministic: every output row is owned by exactly one workgroup.
 #include "kernels.h"
+#include "prof.h"
 
 namespace hydra {
 
@@ -301,14 +302,18 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
                            hipStream_t stream) {
   const int64_t pairs = (int64_t)a.nq * a.H;
   const int64_t blocks = (pairs * 16 + 255) / 256;
+  int tok = prof_begin("bwd_pre", stream);
   hipLaunchKernelGGL(bwd_pre_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a.o, a.dO, a.Dvec,
                      a.nq, a.H);
+  prof_end(tok, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (n_qitems > 0) {
     AttnArgs b = a;
     b.n_items = n_qitems;
+    tok = prof_begin("bwd_dq", stream);
     hipLaunchKernelGGL(bwd_dq_kernel, dim3(n_qitems * a.H), dim3(256), 0, stream, b);
+    prof_end(tok, stream);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -316,7 +321,9 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
     AttnArgs b = a;
     b.items = kitems;
     b.n_items = n_kitems;
+    tok = prof_begin("bwd_dkdv", stream);
     hipLaunchKernelGGL(bwd_dkdv_kernel, dim3(n_kitems * a.H), dim3(256), 0, stream, b);
+    prof_end(tok, stream);
     e = hipGetLastError();
   }
   return e;

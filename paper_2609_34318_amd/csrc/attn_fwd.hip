@@ -9,6 +9,7 @@
 // rounding.  Only tiles that straddle a document start, the causal diagonal or the end
 // of a range evaluate the mask (Sec. 2.2); every other visited tile is fully visible.
 #include "kernels.h"
+#include "prof.h"
 
 namespace hydra {
 
@@ -147,7 +148,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
 
 hipError_t launch_attn_fwd(const AttnArgs& a, uint16_t* o_bf16, hipStream_t stream) {
   if (a.n_items == 0) return hipSuccess;
+  const int tok = prof_begin("attn_fwd", stream);
   hipLaunchKernelGGL(attn_fwd_kernel, dim3(a.n_items * a.H), dim3(256), 0, stream, a, o_bf16);
+  prof_end(tok, stream);
   return hipGetLastError();
 }
 

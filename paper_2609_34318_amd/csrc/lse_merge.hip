@@ -3,6 +3,7 @@
 //   w_x = e^(Lx - L).  Two empty partials (LSE = -inf) stay (0, -inf) with no NaN.
 // HBM-bound: 32 lanes per (row, head), each moving 4 fp32 of O_acc and O_part.
 #include "kernels.h"
+#include "prof.h"
 
 namespace hydra {
 
@@ -47,8 +48,10 @@ hipError_t launch_lse_merge(int64_t n_rows, int H, float* o_acc, float* lse_acc,
                             const float* lse_part, uint16_t* o_bf16, hipStream_t stream) {
   const int64_t threads = n_rows * H * 32;
   const int64_t blocks = (threads + 255) / 256;
+  const int tok = prof_begin("lse_merge", stream);
   hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, n_rows, H, o_acc, lse_acc,
                      o_part, lse_part, o_bf16);
+  prof_end(tok, stream);
   return hipGetLastError();
 }
 

@@ -37,6 +37,14 @@ class ProblemC(ctypes.Structure):
                 ("kv", Chunk)]
 
 
+class KernelStat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32),
+                ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double),
+                ("min_ms", ctypes.c_double),
+                ("max_ms", ctypes.c_double)]
+
+
 class HydraError(RuntimeError):
     def __init__(self, status: int, what: str):
         super().__init__(f"{what} failed: status {status} ({lib().hydra_strerror(status).decode()})")
@@ -72,6 +80,10 @@ def lib() -> ctypes.CDLL:
         L.hydra_plan_items.restype = ctypes.c_int64
         L.hydra_tile_rows.argtypes = [ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
         L.hydra_tile_rows.restype = None
+        L.hydra_profile_start.argtypes = []
+        L.hydra_profile_start.restype = ctypes.c_int
+        L.hydra_profile_stop.argtypes = [ctypes.POINTER(KernelStat), ctypes.c_int32]
+        L.hydra_profile_stop.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -178,3 +190,22 @@ def lse_merge(o_acc, lse_acc, o_part, lse_part, o_bf16=None, stream=None):
     n_rows, n_heads, d_v = o_acc.shape
     _check(lib().hydra_lse_merge(n_rows, n_heads, d_v, _ptr(o_acc), _ptr(lse_acc), _ptr(o_part),
                                  _ptr(lse_part), _ptr(o_bf16), _stream(stream)), "hydra_lse_merge")
+
+
+def profile_start():
+    """Start timing every kernel the library launches (HIP events on the launch stream)."""
+    _check(lib().hydra_profile_start(), "hydra_profile_start")
+
+
+def profile_stop() -> dict:
+    """Stop timing; returns {kernel: {launches, total_ms, min_ms, max_ms, avg_ms}}."""
+    buf = (KernelStat * 16)()
+    n = lib().hydra_profile_stop(buf, 16)
+    if n < 0:
+        raise HydraError(n, "hydra_profile_stop")
+    out = {}
+    for i in range(min(n, 16)):
+        k = buf[i]
+        out[k.name.decode()] = dict(launches=k.launches, total_ms=k.total_ms, min_ms=k.min_ms,
+                                    max_ms=k.max_ms, avg_ms=k.total_ms / max(k.launches, 1))
+    return out

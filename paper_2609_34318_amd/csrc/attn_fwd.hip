@@ -1,29 +1,52 @@
 // Forward partial of one ring step: O = softmax(scale * Q K^T, masked) V and its LSE.
 //
 // One workgroup = 4 waves = 128 query rows of one head; each wave owns 32 rows and keeps
-// them in registers as MFMA B operands for the whole key loop.  Key/value tiles of 64
-// rows are staged through LDS.  Scores are computed transposed (S^T = K Q^T), so every
-// lane holds one query and the softmax row reductions stay in-lane plus one exchange
-// with the lane 32 away.  The running max / sum update is the standard online softmax
-// that FlashAttention uses (named in Sec. 1 and Sec. 3.5); the result is exact up to
-// rounding.  Only tiles that straddle a document start, the causal diagonal or the end
-// of a range evaluate the mask (Sec. 2.2); every other visited tile is fully visible.
+// them in registers as MFMA B operands for the whole key loop.  Key/value tiles of 64 rows
+// stream through two swizzled LDS stages filled by direct global->LDS copies: the copy of
+// tile t+1 is in flight while tile t is computed, one barrier per tile.  Two workgroups
+// share a CU (2 x 80 KB of LDS), so one's softmax overlaps the other's matrix work.
+// Scores are computed transposed (S^T = K Q^T), so every lane holds one query and the
+// softmax row reductions stay in-lane plus one exchange with the lane 32 away.
+//
+// The running max / sum update is the online softmax that FlashAttention uses (named in
+// Sec. 1 and Sec. 3.5), with one liberty: the reference max m only moves when a tile's max
+// exceeds it by more than 8 (log2 units), so O is rescaled rarely.  Every term is still
+// exp2(s - m) for the same m in numerator and denominator, so the result is unchanged up to
+// rounding (terms stay <= 2^8).  Only tiles that straddle a document start, the causal
+// diagonal or the end of a range evaluate the mask (Sec. 2.2).
 #include "kernels.h"
 #include "prof.h"
 
 namespace hydra {
 
 constexpr int FWD_BK = 64;
+constexpr int FWD_KBYTES = FWD_BK * DQK * 2;             // 24 KB
+constexpr int FWD_STAGE = FWD_KBYTES + FWD_BK * DV * 2;  // 40 KB
+constexpr float RESCALE_SLACK = 8.0f;
+
+// Starts the copy of key/value tile t into LDS stage t % 2.
+__device__ __forceinline__ void fwd_issue(lds_char* smem, const AttnArgs& a, const TileRanges kr, int t, int koff,
+                                          int voff, int head, int wave) {
+  int row0, pos0, n;
+  tile_at(kr, t, FWD_BK, row0, pos0, n);
+  lds_char* dst = smem + (t & 1) * FWD_STAGE;
+  dma_tile<DQK, FWD_BK>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
+  dma_tile<DV, FWD_BK>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
+}
 
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* __restrict__ o_bf16) {
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[FWD_BK * PITCH_QK];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[FWD_BK * PITCH_V];
+  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * FWD_STAGE];
+  lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m = lane & 31, hh = lane >> 5, g = lane >> 4, gi = lane & 15;
   const int head = blockIdx.x % a.H;
-  const int* it = a.items + (blockIdx.x / a.H) * ITEM_INTS;
-  const int q_row0 = it[0], q_pos0 = it[1], q_n = it[2], n_ranges = it[3];
+  const Item it(a.items, blockIdx.x / a.H);
+  const int q_row0 = it.row0, q_pos0 = it.pos0, q_n = it.n;
+  const TileRanges kr = tile_ranges(it, FWD_BK);
+  const int n_tiles = kr.nt;
+
+  lds_clear<256>(smem, 2 * FWD_STAGE, tid);
 
   const int qi = wave * 32 + m;
   const bool q_valid = qi < q_n;
@@ -31,6 +54,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
   const int lo_q = q_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_q)] : 0;
   const int lo_last = a.cu[doc_of(a.cu, a.n_docs, q_pos0 + q_n - 1)];
   const float sl2 = a.scale * LOG2E;
+  const int koff = dma_lane_off<DQK>(a.H, head, wave, lane);
+  const int voff = dma_lane_off<DV>(a.H, head, wave, lane);
 
   bf16x8 qf[DQK / 16];
   {
@@ -42,85 +67,86 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
       qf[t] = __builtin_bit_cast(bf16x8, u);
     }
   }
+  __syncthreads();  // LDS cleared before the first copy lands
+
+  if (n_tiles > 0) fwd_issue(smem, a, kr, 0, koff, voff, head, wave);
 
   f32x16 acc[DV / 32];
 #pragma unroll
   for (int d = 0; d < DV / 32; ++d) acc[d] = f32x16{};
   float m_run = NEG_BIG, l_run = 0.f;
 
-  for (int r = 0; r < n_ranges; ++r) {
-    const int k_row0 = it[4 + 3 * r], k_pos0 = it[5 + 3 * r], k_cnt = it[6 + 3 * r];
-    for (int kt = 0; kt < k_cnt; kt += FWD_BK) {
-      const int kn = min(FWD_BK, k_cnt - kt);
-      const int kpos = k_pos0 + kt;
-      __syncthreads();
-      stage_rows<DQK, PITCH_QK, FWD_BK, 256>(Ks, a.k, k_row0 + kt, kn, a.H, head, tid);
-      stage_rows<DV, PITCH_V, FWD_BK, 256>(Vs, a.v, k_row0 + kt, kn, a.H, head, tid);
-      __syncthreads();
+  const int krow = pi_row(m);                    // + 32*kb
+  const int vrow = 8 * hh + (gi >> 2);           // + 16*st
+  const int vcol = 16 * (g & 1) + 4 * (gi & 3);  // + 32*d
 
-      f32x16 s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = f32x16{};
-        const __bf16* krow = Ks + (kb * 32 + pi_row(m)) * PITCH_QK + 8 * hh;
-#pragma unroll
-        for (int t = 0; t < DQK / 16; ++t) s[kb] = mfma(lds_read8(krow + 16 * t), qf[t], s[kb]);
-      }
+  for (int t = 0; t < n_tiles; ++t) {
+    int k_row0, kpos, kn;
+    tile_at(kr, t, FWD_BK, k_row0, kpos, kn);
+    wait_dma();
+    __syncthreads();
+    if (t + 1 < n_tiles) fwd_issue(smem, a, kr, t + 1, koff, voff, head, wave);
+    const lds_char* Ks = smem + (t & 1) * FWD_STAGE;
+    const lds_char* Vs = Ks + FWD_KBYTES;
 
-      const bool full = (kn == FWD_BK) && (lo_last <= kpos) && (kpos + FWD_BK - 1 <= q_pos0);
-      float mx = m_run;
-      if (full) {
+    f32x16 s[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x16{};
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            s[kb][e] *= sl2;
-            mx = fmax2(mx, s[kb][e]);
-          }
-      } else {
+      for (int t2 = 0; t2 < DQK / 16; ++t2)
+        s[kb] = mfma(lds_ld16(Ks, tile_off<DQK, FWD_BK>(32 * kb + krow, 2 * t2 + hh)), qf[t2], s[kb]);
+    }
+
+    const bool full = (kn == FWD_BK) && (lo_last <= kpos) && (kpos + FWD_BK - 1 <= q_pos0);
+    float mx = -INFINITY;
+    if (full) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = kb * 32 + 16 * (e >> 3) + 8 * hh + (e & 7);
-            const int kp = kpos + key;
-            const bool vis = (key < kn) && (kp <= pos_q) && (kp >= lo_q);
-            s[kb][e] = vis ? s[kb][e] * sl2 : -INFINITY;
-            mx = fmax2(mx, s[kb][e]);
-          }
-      }
-      mx = xhalf_max(mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - mx);
-      m_run = mx;
+        for (int e = 0; e < 16; ++e) mx = fmax2(mx, s[kb][e]);
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = kb * 32 + 16 * (e >> 3) + 8 * hh + (e & 7);
+          const int kp = kpos + key;
+          const bool vis = (key < kn) && (kp <= pos_q) && (kp >= lo_q);
+          s[kb][e] = vis ? s[kb][e] : -INFINITY;
+          mx = fmax2(mx, s[kb][e]);
+        }
+    }
+    const float mxs = xhalf_max(mx) * sl2;  // -inf when nothing is visible
+    if (__builtin_amdgcn_ballot_w64(mxs > m_run + RESCALE_SLACK) != 0) {
+      const float m_new = mxs > m_run + RESCALE_SLACK ? mxs : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
       l_run *= alpha;
 #pragma unroll
       for (int d = 0; d < DV / 32; ++d) acc[d] *= alpha;
-
-      bf16x8 pf[4];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        float p[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          p[e] = __builtin_amdgcn_exp2f(s[kb][e] - mx);
-          l_run += p[e];
-        }
-        pf[2 * kb] = to_bf16x8(p);
-        pf[2 * kb + 1] = to_bf16x8(p + 8);
-      }
-
-      // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads.
-#pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        const int vr = 16 * st + 8 * hh + (gi >> 2);
-#pragma unroll
-        for (int d = 0; d < DV / 32; ++d) {
-          const int vc = 32 * d + 16 * (g & 1) + 4 * (gi & 3);
-          const bf16x8 va = lds_read8_tr(Vs + vr * PITCH_V + vc, Vs + (vr + 4) * PITCH_V + vc);
-          acc[d] = mfma(va, pf[st], acc[d]);
-        }
-      }
     }
+    const float neg_m = -m_run;
+
+    bf16x8 pf[4];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      float p[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], sl2, neg_m));
+        l_run += p[e];
+      }
+      pf[2 * kb] = to_bf16x8(p);
+      pf[2 * kb + 1] = to_bf16x8(p + 8);
+    }
+
+    // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads.
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+#pragma unroll
+      for (int d = 0; d < DV / 32; ++d)
+        acc[d] = mfma(lds_tr_frag<DV, FWD_BK>(Vs, 16 * st + vrow, 32 * d + vcol), pf[st], acc[d]);
   }
 
   const float l_tot = xhalf_sum(l_run);

@@ -101,6 +101,167 @@ __device__ __forceinline__ int doc_of(const int* __restrict__ cu, int n_docs, in
   return lo;
 }
 
+// ------------------------------------------------------------------ swizzled LDS tiles
+// Tiles are stored unpadded.  d = 128 tiles: ROWS rows of 256 B.  d = 192 tiles: three
+// column blocks of 64 elements, each ROWS rows of 128 B, so that one 1 KB direct-to-LDS
+// instruction always covers whole rows (4 or 8).  Within a row the 16-byte chunk c lives at
+// chunk c ^ swz(r); the XOR spreads both the 16-byte operand reads (16 rows, one chunk) and
+// the transpose reads (4 rows x 4 chunks) over all 64 LDS banks.
+__device__ __forceinline__ int swz256(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int swz128(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
+
+// Byte offset of logical 16-byte chunk `c` of row `r` in a tile of ROWS rows.
+template <int DIM, int ROWS> __device__ __forceinline__ int tile_off(int r, int c);
+template <> __device__ __forceinline__ int tile_off<128, 64>(int r, int c) { return r * 256 + ((c ^ swz256(r)) << 4); }
+template <> __device__ __forceinline__ int tile_off<128, 32>(int r, int c) { return r * 256 + ((c ^ swz256(r)) << 4); }
+template <> __device__ __forceinline__ int tile_off<192, 64>(int r, int c) {
+  return (c >> 3) * (64 * 128) + r * 128 + (((c & 7) ^ swz128(r)) << 4);
+}
+template <> __device__ __forceinline__ int tile_off<192, 32>(int r, int c) {
+  return (c >> 3) * (32 * 128) + r * 128 + (((c & 7) ^ swz128(r)) << 4);
+}
+
+__device__ __forceinline__ bf16x8 lds_ld16(const lds_char* base, int off) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(base + off);
+}
+
+__device__ __forceinline__ i16x4 lds_tr8(const lds_char* base, int off) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(base + off));
+}
+
+// Transposed operand fragment: each lane points at row `row` (and row + 4) and element
+// column `col`; the transpose read hands lane i of each 16-lane group one column of the
+// 4 x 16 block its group addressed (see the header comment).
+template <int DIM, int ROWS>
+__device__ __forceinline__ bf16x8 lds_tr_frag(const lds_char* base, int row, int col) {
+  const int c = col >> 3, w = (col & 7) << 1;
+  i16x4 lo = lds_tr8(base, tile_off<DIM, ROWS>(row, c) + w);
+  i16x4 hi = lds_tr8(base, tile_off<DIM, ROWS>(row + 4, c) + w);
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// ------------------------------------------------------------------ direct global -> LDS copies
+// A buffer resource is built per tile with its base at the tile's first row and its record
+// count ending at the tile's last valid row, so rows past the end are out of range for the
+// hardware bounds check and never touch memory (all of the offset travels in the VGPR
+// operand, which is what the check covers) (the kernels mask those rows and clear LDS
+// once at start, so whatever the copy leaves there is finite).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* g, int64_t row0, int valid, int H,
+                                                            int dim) {
+  const uint16_t* base = g + row0 * H * (int64_t)dim;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, valid * H * dim * 2, 0x00020000);
+}
+
+// Per-lane byte offset (tile-independent) for dma_tile with 4 waves.  Lane L of wave w writes
+// bytes [16L, 16L+16) of each 1 KB instruction, which holds rows 4j..4j+3 (d = 128) or
+// 8j..8j+7 of one column block (d = 192), j = w + 4i; it fetches the logical chunk the
+// swizzle places there.
+template <int DIM> __device__ __forceinline__ int dma_lane_off(int H, int head, int wave, int lane);
+template <> __device__ __forceinline__ int dma_lane_off<128>(int H, int head, int wave, int lane) {
+  const int q = lane >> 4;
+  const int lc = (lane & 15) ^ ((q << 2) | (wave & 3));
+  return (((4 * wave + q) * H + head) * 128 + lc * 8) * 2;
+}
+template <> __device__ __forceinline__ int dma_lane_off<192>(int H, int head, int wave, int lane) {
+  const int q = lane >> 3;
+  const int lc = (lane & 7) ^ ((((q >> 1) & 1) << 2) | ((wave & 1) << 1) | (q >> 2));
+  return (((8 * wave + q) * H + head) * 192 + lc * 8) * 2;
+}
+
+template <int DIM, int ROWS>
+__device__ __forceinline__ void dma_tile(lds_char* lds, __amdgpu_buffer_rsrc_t rs, int voff, int H, int wave) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  if constexpr (DIM == 128) {
+    constexpr int NINS = ROWS / 4;
+    static_assert(NINS % 4 == 0, "tile must split evenly over 4 waves");
+#pragma unroll
+    for (int i = 0; i < NINS / 4; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + (wave + 4 * i) * 1024), 16,
+                                               voff + 16 * i * H * 256, 0, 0, 0);
+  } else {
+    constexpr int NINS = ROWS / 8;  // per column block
+    static_assert(NINS % 4 == 0, "tile must split evenly over 4 waves");
+#pragma unroll
+    for (int b = 0; b < 3; ++b)
+#pragma unroll
+      for (int i = 0; i < NINS / 4; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + b * ROWS * 128 + (wave + 4 * i) * 1024), 16,
+                                                 voff + 32 * i * H * 384 + b * 128, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Clears `bytes` (multiple of 16 * threads) of LDS.
+template <int THREADS>
+__device__ __forceinline__ void lds_clear(lds_char* lds, int bytes, int tid) {
+  for (int o = tid * 16; o < bytes; o += THREADS * 16)
+    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(lds + o) = u32x4{0u, 0u, 0u, 0u};
+}
+
+// A work item (16 ints, see the plan), read once into scalar registers.  Plain scalar
+// members only: an array here would be placed in scratch memory and indexed dynamically.
+struct Item {
+  int row0, pos0, n, nr;
+  int r0, p0, c0, r1, p1, c1, r2, p2, c2, r3, p3, c3;
+
+  __device__ __forceinline__ Item(const int* items, int idx) {
+    const int* s = items + idx * ITEM_INTS;
+    row0 = __builtin_amdgcn_readfirstlane(s[0]);
+    pos0 = __builtin_amdgcn_readfirstlane(s[1]);
+    n = __builtin_amdgcn_readfirstlane(s[2]);
+    nr = __builtin_amdgcn_readfirstlane(s[3]);
+    r0 = __builtin_amdgcn_readfirstlane(s[4]);
+    p0 = __builtin_amdgcn_readfirstlane(s[5]);
+    c0 = nr > 0 ? __builtin_amdgcn_readfirstlane(s[6]) : 0;
+    r1 = __builtin_amdgcn_readfirstlane(s[7]);
+    p1 = __builtin_amdgcn_readfirstlane(s[8]);
+    c1 = nr > 1 ? __builtin_amdgcn_readfirstlane(s[9]) : 0;
+    r2 = __builtin_amdgcn_readfirstlane(s[10]);
+    p2 = __builtin_amdgcn_readfirstlane(s[11]);
+    c2 = nr > 2 ? __builtin_amdgcn_readfirstlane(s[12]) : 0;
+    r3 = __builtin_amdgcn_readfirstlane(s[13]);
+    p3 = __builtin_amdgcn_readfirstlane(s[14]);
+    c3 = nr > 3 ? __builtin_amdgcn_readfirstlane(s[15]) : 0;
+  }
+};
+
+// The ranges of a work item cut into tiles of B rows (the last tile of a range may be short).
+// A value type of scalars: pass it by value and never take its address, so that it stays in
+// scalar registers (a select between fields of a struct in memory becomes a scratch load
+// with a dynamic index).
+struct TileRanges {
+  int r0, p0, c0, r1, p1, c1, r2, p2, c2, r3, p3, c3;
+  int f1, f2, f3, nt;  // first tile of ranges 1..3, total tiles
+};
+
+__device__ __forceinline__ TileRanges tile_ranges(const Item& it, int B) {
+  TileRanges R;
+  R.r0 = it.r0; R.p0 = it.p0; R.c0 = it.c0;
+  R.r1 = it.r1; R.p1 = it.p1; R.c1 = it.c1;
+  R.r2 = it.r2; R.p2 = it.p2; R.c2 = it.c2;
+  R.r3 = it.r3; R.p3 = it.p3; R.c3 = it.c3;
+  R.f1 = (R.c0 + B - 1) / B;
+  R.f2 = R.f1 + (R.c1 + B - 1) / B;
+  R.f3 = R.f2 + (R.c2 + B - 1) / B;
+  R.nt = R.f3 + (R.c3 + B - 1) / B;
+  return R;
+}
+
+// Rows [row0, row0 + n) at global positions [pos0, pos0 + n) of tile t < R.nt.
+__device__ __forceinline__ void tile_at(const TileRanges R, int t, int B, int& row0, int& pos0, int& n) {
+  int rr = R.r0, pp = R.p0, cc = R.c0, ff = 0;
+  if (t >= R.f1) { rr = R.r1; pp = R.p1; cc = R.c1; ff = R.f1; }
+  if (t >= R.f2) { rr = R.r2; pp = R.p2; cc = R.c2; ff = R.f2; }
+  if (t >= R.f3) { rr = R.r3; pp = R.p3; cc = R.c3; ff = R.f3; }
+  const int off = (t - ff) * B;
+  row0 = rr + off;
+  pos0 = pp + off;
+  n = min(B, cc - off);
+}
+
 // Stage `rows` rows (of at most 32*n_sub) of a [token][head][dim] bf16 tensor into an LDS
 // tile with the given pitch; rows beyond `valid` are zero-filled.
 template <int DIM, int PITCH, int ROWS, int THREADS>

@@ -98,6 +98,7 @@ AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
   a.cu = reinterpret_cast<const int*>(base + w.cu_off);
   a.items = reinterpret_cast<const int*>(base + w.qitems_off);
   a.Dvec = reinterpret_cast<float*>(base + w.d_off);
+  a.lse2 = reinterpret_cast<float*>(base + w.lse2_off);
   a.n_docs = int(pr.cu.size()) - 1;
   a.H = pr.H;
   a.nq = int(pr.nq);

@@ -2,11 +2,13 @@
 //   D_i = <dO_i, O_i>,  P = exp(S - LSE),  dV += P^T dO,  dS = P o (dO V^T - D),
 //   dK += scale dS^T Q,  dQ += scale dS K.
 // Three kernels:
-//   bwd_pre   D = rowsum(dO o O)                                  (HBM-bound)
+//   bwd_pre   D = rowsum(dO o O) and LSE * log2(e)                  (HBM-bound)
 //   bwd_dq    query-stationary: recomputes S^T and dP^T per key tile, accumulates dQ^T
 //   bwd_dkdv  key-stationary: recomputes S and dP per query tile, accumulates dK^T, dV^T
 // Splitting dQ from dK/dV recomputes S and dP once more but needs no atomics and is
-// deterministic: every output row is owned by exactly one workgroup.
+// deterministic: every output row is owned by exactly one workgroup.  Both main kernels
+// stream their other-side tiles through swizzled LDS stages filled by direct
+// buffer->LDS copies issued ahead of use.
 #include "kernels.h"
 #include "prof.h"
 
@@ -15,7 +17,9 @@ namespace hydra {
 // ------------------------------------------------------------------ D = rowsum(dO * O)
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict__ o,
                                                       const uint16_t* __restrict__ dO,
-                                                      float* __restrict__ D, int nq, int H) {
+                                                      const float* __restrict__ lse,
+                                                      float* __restrict__ D, float* __restrict__ lse2,
+                                                      int nq, int H) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t rh = gid >> 4;  // (row, head) pair, 16 lanes each
   const int sub = threadIdx.x & 15;
@@ -36,24 +40,40 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict
   acc += __shfl_xor(acc, 1, 16);
   if (ok && sub == 0) {
     const int row = (int)(rh / H), head = (int)(rh % H);
-    D[(int64_t)head * nq + row] = acc;
+    const int64_t li = (int64_t)head * nq + row;
+    D[li] = acc;
+    lse2[li] = lse[li] * LOG2E;
   }
 }
 
 // ------------------------------------------------------------------ dQ (query-stationary)
 constexpr int DQ_BK = 64;
+constexpr int DQ_KBYTES = DQ_BK * DQK * 2;            // 24 KB
+constexpr int DQ_STAGE = DQ_KBYTES + DQ_BK * DV * 2;  // 40 KB
 
-__global__ __launch_bounds__(256, 1) void bwd_dq_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) __bf16 Ks[DQ_BK * PITCH_QK];
-  __shared__ __attribute__((aligned(16))) __bf16 Vs[DQ_BK * PITCH_V];
+__device__ __forceinline__ void dq_issue(lds_char* smem, const AttnArgs& a, const TileRanges kr, int t, int koff,
+                                         int voff, int wave) {
+  int row0, pos0, n;
+  tile_at(kr, t, DQ_BK, row0, pos0, n);
+  lds_char* dst = smem + (t & 1) * DQ_STAGE;
+  dma_tile<DQK, DQ_BK>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
+  dma_tile<DV, DQ_BK>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
+}
+
+__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * DQ_STAGE];
+  lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m = lane & 31, hh = lane >> 5, g = lane >> 4, gi = lane & 15;
   const int head = blockIdx.x % a.H;
-  const int* it = a.items + (blockIdx.x / a.H) * ITEM_INTS;
-  const int q_row0 = it[0], q_pos0 = it[1], q_n = it[2], n_ranges = it[3];
-  if (n_ranges == 0) return;  // uniform over the workgroup
+  const Item it(a.items, blockIdx.x / a.H);
+  const TileRanges kr = tile_ranges(it, DQ_BK);
+  const int n_tiles = kr.nt;
+  if (n_tiles == 0) return;  // uniform over the workgroup
+  const int q_row0 = it.row0, q_pos0 = it.pos0, q_n = it.n;
 
+  lds_clear<256>(smem, 2 * DQ_STAGE, tid);
   const int qi = wave * 32 + m;
   const bool q_valid = qi < q_n;
   const int pos_q = q_valid ? q_pos0 + qi : -1;
@@ -62,8 +82,10 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(AttnArgs a) {
   const float sl2 = a.scale * LOG2E;
   const int64_t qrow = q_row0 + (q_valid ? qi : 0);
   // invalid rows: LSE = +inf makes P = 0, D = 0 keeps dS = 0
-  const float lse2 = q_valid ? a.lse[(int64_t)head * a.nq + qrow] * LOG2E : INFINITY;
+  const float lse2 = q_valid ? a.lse2[(int64_t)head * a.nq + qrow] : INFINITY;
   const float Dq = q_valid ? a.Dvec[(int64_t)head * a.nq + qrow] : 0.f;
+  const int koff = dma_lane_off<DQK>(a.H, head, wave, lane);
+  const int voff = dma_lane_off<DV>(a.H, head, wave, lane);
 
   bf16x8 qf[DQK / 16], df[DV / 16];
   {
@@ -82,58 +104,65 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(AttnArgs a) {
       df[t] = __builtin_bit_cast(bf16x8, u);
     }
   }
+  __syncthreads();  // LDS cleared before the first copy lands
+  dq_issue(smem, a, kr, 0, koff, voff, wave);
 
   f32x16 acc[DQK / 32];
 #pragma unroll
   for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  for (int r = 0; r < n_ranges; ++r) {
-    const int k_row0 = it[4 + 3 * r], k_pos0 = it[5 + 3 * r], k_cnt = it[6 + 3 * r];
-    for (int kt = 0; kt < k_cnt; kt += DQ_BK) {
-      const int kn = min(DQ_BK, k_cnt - kt);
-      const int kpos = k_pos0 + kt;
-      __syncthreads();
-      stage_rows<DQK, PITCH_QK, DQ_BK, 256>(Ks, a.k, k_row0 + kt, kn, a.H, head, tid);
-      stage_rows<DV, PITCH_V, DQ_BK, 256>(Vs, a.v, k_row0 + kt, kn, a.H, head, tid);
-      __syncthreads();
-      const bool full = (kn == DQ_BK) && (lo_last <= kpos) && (kpos + DQ_BK - 1 <= q_pos0);
+  const int arow = pi_row(m);                    // + 32*kb
+  const int trow = 8 * hh + (gi >> 2);           // + 32*kb + 16*half
+  const int tcol = 16 * (g & 1) + 4 * (gi & 3);  // + 32*c
 
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        f32x16 s = f32x16{}, dp = f32x16{};
-        const __bf16* krow = Ks + (kb * 32 + pi_row(m)) * PITCH_QK + 8 * hh;
-        const __bf16* vrow = Vs + (kb * 32 + pi_row(m)) * PITCH_V + 8 * hh;
-#pragma unroll
-        for (int t = 0; t < DQK / 16; ++t) s = mfma(lds_read8(krow + 16 * t), qf[t], s);
-#pragma unroll
-        for (int t = 0; t < DV / 16; ++t) dp = mfma(lds_read8(vrow + 16 * t), df[t], dp);
+  for (int t = 0; t < n_tiles; ++t) {
+    int k_row0, kpos, kn;
+    tile_at(kr, t, DQ_BK, k_row0, kpos, kn);
+    wait_dma();
+    barrier_lds();
+    if (t + 1 < n_tiles) dq_issue(smem, a, kr, t + 1, koff, voff, wave);
+    const lds_char* Ks = smem + (t & 1) * DQ_STAGE;
+    const lds_char* Vs = Ks + DQ_KBYTES;
+    const bool full = (kn == DQ_BK) && (lo_last <= kpos) && (kpos + DQ_BK - 1 <= q_pos0);
 
-        float ds[16];
+#pragma unroll 1
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float p = __builtin_amdgcn_exp2f(s[e] * sl2 - lse2);
-          if (!full) {
-            const int key = kb * 32 + 16 * (e >> 3) + 8 * hh + (e & 7);
-            const int kp = kpos + key;
-            const bool vis = (key < kn) && (kp <= pos_q) && (kp >= lo_q);
-            p = vis ? p : 0.f;
-          }
-          ds[e] = p * (dp[e] - Dq);
+      for (int t2 = 0; t2 < DQK / 16; ++t2)
+        s = mfma(lds_ld16(Ks, tile_off<DQK, DQ_BK>(32 * kb + arow, 2 * t2 + hh)), qf[t2], s);
+#pragma unroll
+      for (int t2 = 0; t2 < DV / 16; ++t2)
+        dp = mfma(lds_ld16(Vs, tile_off<DV, DQ_BK>(32 * kb + arow, 2 * t2 + hh)), df[t2], dp);
+
+      float ds[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse2));
+        if (!full) {
+          const int key = kb * 32 + 16 * (e >> 3) + 8 * hh + (e & 7);
+          const int kp = kpos + key;
+          const bool vis = (key < kn) && (kp <= pos_q) && (kp >= lo_q);
+          p = vis ? p : 0.f;
         }
-        const bf16x8 dsf0 = to_bf16x8(ds), dsf1 = to_bf16x8(ds + 8);
-
-        // dQ^T[c][q] += K^T[c][key] dS^T[key][q]; K^T fragments via LDS transpose reads.
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int kr = kb * 32 + 16 * half + 8 * hh + (gi >> 2);
-#pragma unroll
-          for (int c = 0; c < DQK / 32; ++c) {
-            const int kc = 32 * c + 16 * (g & 1) + 4 * (gi & 3);
-            const bf16x8 ka = lds_read8_tr(Ks + kr * PITCH_QK + kc, Ks + (kr + 4) * PITCH_QK + kc);
-            acc[c] = mfma(ka, half ? dsf1 : dsf0, acc[c]);
-          }
-        }
+        ds[e] = p * (dp[e] - Dq);
       }
+      const bf16x8 dsf0 = to_bf16x8(ds), dsf1 = to_bf16x8(ds + 8);
+
+      // dQ^T[c][q] += K^T[c][key] dS^T[key][q]; K^T fragments via LDS transpose reads,
+      // three column blocks at a time (the products of one group run while the next loads).
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int c0 = 0; c0 < DQK / 32; c0 += 3) {
+          bf16x8 f[3];
+#pragma unroll
+          for (int j = 0; j < 3; ++j)
+            f[j] = lds_tr_frag_async<DQK, DQ_BK>(Ks, 32 * kb + 16 * half + trow, 32 * (c0 + j) + tcol);
+          lds_wait(f[0], f[1], f[2]);
+#pragma unroll
+          for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[j], half ? dsf1 : dsf0, acc[c0 + j]);
+        }
     }
   }
 
@@ -155,49 +184,87 @@ __global__ __launch_bounds__(256, 1) void bwd_dq_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------ dK, dV (key-stationary)
-constexpr int KV_BQ = 32;
+constexpr int KV_BQ = 64;                                 // query rows per stage
+constexpr int KV_QBYTES = KV_BQ * DQK * 2;                // 24 KB
+constexpr int KV_OBYTES = KV_BQ * DV * 2;                 // 16 KB
+constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_BQ * 4;  // + LSE2 and D
+constexpr int KV_NSTAGE = 3;
+// Vector-memory instructions one kv_issue adds per wave: 6 (Q) + 4 (dO) copies, plus one
+// vector copy on waves 0 and 1.  Waiting for vmcnt <= 10 therefore completes tile t while
+// tile t+1 may stay in flight (waves 0 and 1 also finish one of t+1's copies).
+constexpr int KV_VMCNT_ONE_TILE = 10;
+
+__device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, const TileRanges qr, int t, int qoff,
+                                         int ooff, int head, int wave, int lane) {
+  int row0, pos0, n;
+  tile_at(qr, t, KV_BQ, row0, pos0, n);
+  lds_char* dst = smem + (t % KV_NSTAGE) * KV_STAGE;
+  dma_tile<DQK, KV_BQ>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff, a.H, wave);
+  dma_tile<DV, KV_BQ>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff, a.H, wave);
+  const int64_t li = (int64_t)head * a.nq + row0;
+  if (wave == 0) dma_vec64(dst + KV_QBYTES + KV_OBYTES, a.lse2 + li, n, lane);
+  if (wave == 1) dma_vec64(dst + KV_QBYTES + KV_OBYTES + KV_BQ * 4, a.Dvec + li, n, lane);
+}
 
 __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) __bf16 Qs[KV_BQ * PITCH_QK];
-  __shared__ __attribute__((aligned(16))) __bf16 dOs[KV_BQ * PITCH_V];
-  __shared__ __attribute__((aligned(16))) float lse_s[KV_BQ];
-  __shared__ __attribute__((aligned(16))) float D_s[KV_BQ];
+  __shared__ __attribute__((aligned(1024))) char smem_raw[KV_NSTAGE * KV_STAGE];
+  lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m = lane & 31, hh = lane >> 5, g = lane >> 4, gi = lane & 15;
   const int head = blockIdx.x % a.H;
-  const int* it = a.items + (blockIdx.x / a.H) * ITEM_INTS;
-  const int k_row0 = it[0], k_pos0 = it[1], k_n = it[2], n_ranges = it[3];
-  if (n_ranges == 0) return;  // uniform over the workgroup
+  const Item it(a.items, blockIdx.x / a.H);
+  const TileRanges qr = tile_ranges(it, KV_BQ);
+  const int n_tiles = qr.nt;
+  if (n_tiles == 0) return;  // uniform over the workgroup
+  const int k_row0 = it.row0, k_pos0 = it.pos0, k_n = it.n;
 
+  lds_clear<256>(smem, KV_NSTAGE * KV_STAGE, tid);
   const int kj = wave * 32 + m;
   const bool k_valid = kj < k_n;
   const int pos_k = k_valid ? k_pos0 + kj : 0x7fffffff;
-  const int hi_k = k_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_k) + 1] : 0;
+  int hi_k = k_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_k) + 1] : 0;
+  // finish these loads here: left pending, the tile loop would wait for all copies in flight
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(hi_k)::"memory");
   const int kn_w = min(32, max(0, k_n - wave * 32));  // valid keys of this wave
   const int wk_first = k_pos0 + wave * 32;
   const int wk_last = wk_first + kn_w - 1;
-  const int hi_first = kn_w > 0 ? a.cu[doc_of(a.cu, a.n_docs, wk_first) + 1] : 0;
+  const int hi_first =
+      __builtin_amdgcn_readfirstlane(kn_w > 0 ? a.cu[doc_of(a.cu, a.n_docs, wk_first) + 1] : 0);
   const float sl2 = a.scale * LOG2E;
   const int64_t krow = k_row0 + (k_valid ? kj : 0);
+  const int qoff = dma_lane_off<DQK>(a.H, head, wave, lane);
+  const int ooff = dma_lane_off<DV>(a.H, head, wave, lane);
 
   bf16x8 kf[DQK / 16], vf[DV / 16];
   {
     const uint16_t* kp = a.k + (krow * a.H + head) * DQK + 8 * hh;
     const uint16_t* vp = a.v + (krow * a.H + head) * DV + 8 * hh;
+    u32x4 uk[DQK / 16], uv[DV / 16];
+#pragma unroll
+    for (int t = 0; t < DQK / 16; ++t) uk[t] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int t = 0; t < DV / 16; ++t) uv[t] = u32x4{0u, 0u, 0u, 0u};
+    if (k_valid) {
+#pragma unroll
+      for (int t = 0; t < DQK / 16; ++t) uk[t] = ldg16_asm(kp + 16 * t);
+#pragma unroll
+      for (int t = 0; t < DV / 16; ++t) uv[t] = ldg16_asm(vp + 16 * t);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
     for (int t = 0; t < DQK / 16; ++t) {
-      u32x4 u = {0u, 0u, 0u, 0u};
-      if (k_valid) u = ldg16(kp + 16 * t);
-      kf[t] = __builtin_bit_cast(bf16x8, u);
+      asm volatile("" : "+v"(uk[t]));  // order every use after the wait above
+      kf[t] = __builtin_bit_cast(bf16x8, uk[t]);
     }
 #pragma unroll
     for (int t = 0; t < DV / 16; ++t) {
-      u32x4 u = {0u, 0u, 0u, 0u};
-      if (k_valid) u = ldg16(vp + 16 * t);
-      vf[t] = __builtin_bit_cast(bf16x8, u);
+      asm volatile("" : "+v"(uv[t]));
+      vf[t] = __builtin_bit_cast(bf16x8, uv[t]);
     }
   }
+  __syncthreads();  // LDS cleared before the first copies land
+  for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head, wave, lane);
 
   f32x16 accK[DQK / 32], accV[DV / 32];
 #pragma unroll
@@ -205,64 +272,84 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
   for (int d = 0; d < DV / 32; ++d) accV[d] = f32x16{};
 
-  for (int r = 0; r < n_ranges; ++r) {
-    const int q_row0 = it[4 + 3 * r], q_pos0 = it[5 + 3 * r], q_cnt = it[6 + 3 * r];
-    for (int qt = 0; qt < q_cnt; qt += KV_BQ) {
-      const int qn = min(KV_BQ, q_cnt - qt);
-      const int qpos = q_pos0 + qt;
-      __syncthreads();
-      stage_rows<DQK, PITCH_QK, KV_BQ, 256>(Qs, a.q, q_row0 + qt, qn, a.H, head, tid);
-      stage_rows<DV, PITCH_V, KV_BQ, 256>(dOs, a.dO, q_row0 + qt, qn, a.H, head, tid);
-      if (tid < KV_BQ) {
-        const int64_t row = q_row0 + qt + tid;
-        lse_s[tid] = tid < qn ? a.lse[(int64_t)head * a.nq + row] * LOG2E : INFINITY;
-        D_s[tid] = tid < qn ? a.Dvec[(int64_t)head * a.nq + row] : 0.f;
-      }
-      __syncthreads();
-      if (kn_w == 0) continue;  // wave-uniform; barriers above are still reached
+  const int arow = pi_row(m);                    // + 32*sb
+  const int trow = 8 * hh + (gi >> 2);           // + 32*sb + 16*half
+  const int tcol = 16 * (g & 1) + 4 * (gi & 3);  // + 32*c
 
+  for (int t = 0; t < n_tiles; ++t) {
+    int q_row0, qpos, qn;
+    tile_at(qr, t, KV_BQ, q_row0, qpos, qn);
+    // copies of tile t are done once at most one later tile's copies are still in flight
+    if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
+    else wait_dma();
+    barrier_lds();
+    if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head, wave, lane);
+    if (kn_w == 0) continue;  // wave-uniform; the barrier above is still reached
+    const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
+    const lds_char* Os = Qs + KV_QBYTES;
+    const lds_char* vec_s = Qs + KV_QBYTES + KV_OBYTES;  // LSE2[64] then D[64]
+
+#pragma unroll 1
+    for (int sb = 0; sb < KV_BQ / 32; ++sb) {
+      const int qb = qpos + 32 * sb;
       f32x16 s = f32x16{}, dp = f32x16{};
-      {
-        const __bf16* qr = Qs + pi_row(m) * PITCH_QK + 8 * hh;
-        const __bf16* dr = dOs + pi_row(m) * PITCH_V + 8 * hh;
 #pragma unroll
-        for (int t = 0; t < DQK / 16; ++t) s = mfma(lds_read8(qr + 16 * t), kf[t], s);
+      for (int t2 = 0; t2 < DQK / 16; ++t2)
+        s = mfma(lds_ld16(Qs, tile_off<DQK, KV_BQ>(32 * sb + arow, 2 * t2 + hh)), kf[t2], s);
 #pragma unroll
-        for (int t = 0; t < DV / 16; ++t) dp = mfma(lds_read8(dr + 16 * t), vf[t], dp);
-      }
-      const bool full = (kn_w == 32) && (qn == KV_BQ) && (wk_last <= qpos) && (qpos + KV_BQ - 1 < hi_first);
+      for (int t2 = 0; t2 < DV / 16; ++t2)
+        dp = mfma(lds_ld16(Os, tile_off<DV, KV_BQ>(32 * sb + arow, 2 * t2 + hh)), vf[t2], dp);
+
+      const bool full = (kn_w == 32) && (qn >= 32 * (sb + 1)) && (wk_last <= qb) && (qb + 31 < hi_first);
+      // this lane's query rows are 32*sb + 8*hh + {0..7, 16..23}
+      f32x4 l0 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh)), l1 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh + 4));
+      f32x4 l2 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh + 16)), l3 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh + 20));
+      f32x4 d0 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh)), d1 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh + 4));
+      f32x4 d2 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh + 16));
+      f32x4 d3 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh + 20));
+      lds_wait4(l0, l1, l2, l3);
+      lds_wait4(d0, d1, d2, d3);
+      const float lse_r[16] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3],
+                               l2[0], l2[1], l2[2], l2[3], l3[0], l3[1], l3[2], l3[3]};
+      const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
+                             d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};
       float p[16], ds[16];
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int qq = 16 * (e >> 3) + 8 * hh + (e & 7);
-        float pv = __builtin_amdgcn_exp2f(s[e] * sl2 - lse_s[qq]);
+        const int qq = 32 * sb + 16 * (e >> 3) + 8 * hh + (e & 7);
+        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
         if (!full) {
           const int pq = qpos + qq;
           const bool vis = (qq < qn) && (pq >= pos_k) && (pq < hi_k);
           pv = vis ? pv : 0.f;
         }
         p[e] = pv;
-        ds[e] = pv * (dp[e] - D_s[qq]);
+        ds[e] = pv * (dp[e] - D_r[e]);
       }
       const bf16x8 pf0 = to_bf16x8(p), pf1 = to_bf16x8(p + 8);
       const bf16x8 sf0 = to_bf16x8(ds), sf1 = to_bf16x8(ds + 8);
 
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        const int qr = 16 * half + 8 * hh + (gi >> 2);
+        const int r = 32 * sb + 16 * half + trow;
         // dV^T[dv][key] += dO^T[dv][q] P[q][key]
+        {
+          bf16x8 f[4];
 #pragma unroll
-        for (int d = 0; d < DV / 32; ++d) {
-          const int dc = 32 * d + 16 * (g & 1) + 4 * (gi & 3);
-          const bf16x8 da = lds_read8_tr(dOs + qr * PITCH_V + dc, dOs + (qr + 4) * PITCH_V + dc);
-          accV[d] = mfma(da, half ? pf1 : pf0, accV[d]);
+          for (int d = 0; d < DV / 32; ++d) f[d] = lds_tr_frag_async<DV, KV_BQ>(Os, r, 32 * d + tcol);
+          lds_wait(f[0], f[1], f[2], f[3]);
+#pragma unroll
+          for (int d = 0; d < DV / 32; ++d) accV[d] = mfma(f[d], half ? pf1 : pf0, accV[d]);
         }
         // dK^T[c][key] += Q^T[c][q] dS[q][key]
 #pragma unroll
-        for (int c = 0; c < DQK / 32; ++c) {
-          const int qc = 32 * c + 16 * (g & 1) + 4 * (gi & 3);
-          const bf16x8 qa = lds_read8_tr(Qs + qr * PITCH_QK + qc, Qs + (qr + 4) * PITCH_QK + qc);
-          accK[c] = mfma(qa, half ? sf1 : sf0, accK[c]);
+        for (int c0 = 0; c0 < DQK / 32; c0 += 3) {
+          bf16x8 f[3];
+#pragma unroll
+          for (int j = 0; j < 3; ++j) f[j] = lds_tr_frag_async<DQK, KV_BQ>(Qs, r, 32 * (c0 + j) + tcol);
+          lds_wait(f[0], f[1], f[2]);
+#pragma unroll
+          for (int j = 0; j < 3; ++j) accK[c0 + j] = mfma(f[j], half ? sf1 : sf0, accK[c0 + j]);
         }
       }
     }
@@ -303,8 +390,8 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
   const int64_t pairs = (int64_t)a.nq * a.H;
   const int64_t blocks = (pairs * 16 + 255) / 256;
   int tok = prof_begin("bwd_pre", stream);
-  hipLaunchKernelGGL(bwd_pre_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a.o, a.dO, a.Dvec,
-                     a.nq, a.H);
+  hipLaunchKernelGGL(bwd_pre_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a.o, a.dO, a.lse, a.Dvec,
+                     a.lse2, a.nq, a.H);
   prof_end(tok, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -84,7 +84,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
     int k_row0, kpos, kn;
     tile_at(kr, t, FWD_BK, k_row0, kpos, kn);
     wait_dma();
-    __syncthreads();
+    barrier_lds();
     if (t + 1 < n_tiles) fwd_issue(smem, a, kr, t + 1, koff, voff, head, wave);
     const lds_char* Ks = smem + (t & 1) * FWD_STAGE;
     const lds_char* Vs = Ks + FWD_KBYTES;
@@ -141,12 +141,23 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
       pf[2 * kb + 1] = to_bf16x8(p + 8);
     }
 
-    // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads.
+    // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads,
+    // the reads for step st+1 in flight while step st's products run.
+    bf16x8 vf[2][DV / 32];
 #pragma unroll
-    for (int st = 0; st < 4; ++st)
+    for (int d = 0; d < DV / 32; ++d) vf[0][d] = lds_tr_frag_async<DV, FWD_BK>(Vs, vrow, 32 * d + vcol);
 #pragma unroll
-      for (int d = 0; d < DV / 32; ++d)
-        acc[d] = mfma(lds_tr_frag<DV, FWD_BK>(Vs, 16 * st + vrow, 32 * d + vcol), pf[st], acc[d]);
+    for (int st = 0; st < 4; ++st) {
+      bf16x8* cur = vf[st & 1];
+      lds_wait(cur[0], cur[1], cur[2], cur[3]);
+      if (st + 1 < 4) {
+#pragma unroll
+        for (int d = 0; d < DV / 32; ++d)
+          vf[(st + 1) & 1][d] = lds_tr_frag_async<DV, FWD_BK>(Vs, 16 * (st + 1) + vrow, 32 * d + vcol);
+      }
+#pragma unroll
+      for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(cur[d], pf[st], acc[d]);
+    }
   }
 
   const float l_tot = xhalf_sum(l_run);

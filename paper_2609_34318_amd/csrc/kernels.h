@@ -91,6 +91,16 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const float* v) {
 
 __device__ __forceinline__ u32x4 ldg16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
+// 16-byte global load as inline assembly, for operands loaded once before a tile loop whose
+// copies are waited for with partial vmcnt counts: the compiler's wait insertion would
+// otherwise keep such registers "possibly pending" across the loop back edge and wait for
+// every copy in flight before each use.  Complete them with wait_vmem_all() before use.
+__device__ __forceinline__ u32x4 ldg16_asm(const void* p) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+
 // Largest d with cu[d] <= pos (cu has n_docs + 1 entries, pos inside the window).
 __device__ __forceinline__ int doc_of(const int* __restrict__ cu, int n_docs, int pos) {
   int lo = 0, hi = n_docs;
@@ -142,6 +152,50 @@ __device__ __forceinline__ bf16x8 lds_tr_frag(const lds_char* base, int row, int
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// The same transpose read issued as inline assembly.  The compiler's wait insertion treats
+// the builtin as a possible alias of every direct-to-LDS copy still in flight (including
+// the prefetch into the other stage) and waits for all of them first; the asm form is not
+// tracked by that pass, so the caller must wait for it explicitly with lds_wait(), which
+// also ties the fragments to the wait so their consumers cannot move above it.
+__device__ __forceinline__ i16x4 lds_tr8_asm(const lds_char* base, int off) {
+  i16x4 v;
+  const uint32_t addr = (uint32_t)(uintptr_t)(base + off);
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  return v;
+}
+
+template <int DIM, int ROWS>
+__device__ __forceinline__ bf16x8 lds_tr_frag_async(const lds_char* base, int row, int col) {
+  const int c = col >> 3, w = (col & 7) << 1;
+  i16x4 lo = lds_tr8_asm(base, tile_off<DIM, ROWS>(row, c) + w);
+  i16x4 hi = lds_tr8_asm(base, tile_off<DIM, ROWS>(row + 4, c) + w);
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Four floats from LDS as inline assembly (same reason as lds_tr8_asm); wait with lds_wait4.
+__device__ __forceinline__ f32x4 lds_f4_asm(const lds_char* base, int off) {
+  f32x4 v;
+  const uint32_t addr = (uint32_t)(uintptr_t)(base + off);
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  return v;
+}
+__device__ __forceinline__ void lds_wait4(f32x4& a, f32x4& b, f32x4& c, f32x4& d) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d)::"memory");
+}
+
+// Waits for every outstanding LDS read and marks the fragments as produced here.
+__device__ __forceinline__ void lds_wait(bf16x8& a, bf16x8& b, bf16x8& c, bf16x8& d) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d)::"memory");
+}
+__device__ __forceinline__ void lds_wait(bf16x8& a, bf16x8& b) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b)::"memory");
+}
+__device__ __forceinline__ void lds_wait(bf16x8& a, bf16x8& b, bf16x8& c) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c)::"memory");
+}
+
 // ------------------------------------------------------------------ direct global -> LDS copies
 // A buffer resource is built per tile with its base at the tile's first row and its record
 // count ending at the tile's last valid row, so rows past the end are out of range for the
@@ -170,6 +224,15 @@ template <> __device__ __forceinline__ int dma_lane_off<192>(int H, int head, in
   return (((8 * wave + q) * H + head) * 192 + lc * 8) * 2;
 }
 
+// voff + inc, computed where it is used: the compiler would otherwise hoist one VGPR per
+// copy instruction out of the tile loop and, under register pressure, spill them (the
+// reloads then wait on every copy in flight).
+__device__ __forceinline__ int add_here(int voff, int inc) {
+  int o;
+  asm volatile("v_add_u32 %0, %1, %2" : "=v"(o) : "s"(inc), "v"(voff));
+  return o;
+}
+
 template <int DIM, int ROWS>
 __device__ __forceinline__ void dma_tile(lds_char* lds, __amdgpu_buffer_rsrc_t rs, int voff, int H, int wave) {
   typedef __attribute__((address_space(3))) void lds_void;
@@ -179,7 +242,7 @@ __device__ __forceinline__ void dma_tile(lds_char* lds, __amdgpu_buffer_rsrc_t r
 #pragma unroll
     for (int i = 0; i < NINS / 4; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + (wave + 4 * i) * 1024), 16,
-                                               voff + 16 * i * H * 256, 0, 0, 0);
+                                               i == 0 ? voff : add_here(voff, 16 * i * H * 256), 0, 0, 0);
   } else {
     constexpr int NINS = ROWS / 8;  // per column block
     static_assert(NINS % 4 == 0, "tile must split evenly over 4 waves");
@@ -188,11 +251,25 @@ __device__ __forceinline__ void dma_tile(lds_char* lds, __amdgpu_buffer_rsrc_t r
 #pragma unroll
       for (int i = 0; i < NINS / 4; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + b * ROWS * 128 + (wave + 4 * i) * 1024), 16,
-                                                 voff + 32 * i * H * 384 + b * 128, 0, 0, 0);
+                                                 (b == 0 && i == 0) ? voff : add_here(voff, 32 * i * H * 384 + b * 128),
+                                                 0, 0, 0);
   }
 }
 
+// 64 consecutive floats (one per lane) into LDS; entries past `valid` are out of range.
+__device__ __forceinline__ void dma_vec64(lds_char* lds, const float* g, int valid, int lane) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(g), (short)0, valid * 4, 0x00020000);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)lds, 4, lane * 4, 0, 0, 0);
+}
+
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Workgroup barrier for the tile loops: this wave's LDS reads are finished and every wave
+// has arrived.  Copies into LDS are waited for explicitly (wait_dma / vmcnt) before it;
+// unlike __syncthreads it does not also wait for the copies still in flight for later tiles.
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Clears `bytes` (multiple of 16 * threads) of LDS.
 template <int THREADS>
@@ -293,6 +370,7 @@ struct AttnArgs {
   float* dk;
   float* dv;
   float* Dvec;         // bwd: [H][nq] rowsum(dO * O)
+  float* lse2;         // bwd: [H][nq] final LSE * log2(e)
   const int* items;    // work items
   const int* cu;       // document boundaries
   int n_docs;

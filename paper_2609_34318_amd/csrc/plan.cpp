@@ -198,6 +198,8 @@ WsLayout ws_layout(const Problem& pr) {
   off = align_up(off + size_t(nkt) * kItemInts * sizeof(int32_t), 256);
   w.d_off = off;
   off = align_up(off + size_t(pr.H) * size_t(pr.nq) * sizeof(float), 256);
+  w.lse2_off = off;
+  off = align_up(off + size_t(pr.H) * size_t(pr.nq) * sizeof(float), 256);
   w.total = std::max<size_t>(off, 256);
   return w;
 }

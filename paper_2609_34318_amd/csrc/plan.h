@@ -35,7 +35,7 @@ int64_t visible_pairs(const Problem& pr);
 
 // Byte offsets of the workspace regions.
 struct WsLayout {
-  size_t cu_off, qitems_off, kitems_off, d_off, total;
+  size_t cu_off, qitems_off, kitems_off, d_off, lse2_off, total;
   int64_t n_qitems, n_kitems;
 };
 WsLayout ws_layout(const Problem& pr);

@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
   lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int m = lane & 31, hh = lane >> 5, g = lane >> 4, gi = lane & 15;
+  const int m = lane & 31, hh = lane >> 5;
   const int head = blockIdx.x % a.H;
   const Item it(a.items, blockIdx.x / a.H);
   const TileRanges kr = tile_ranges(it, DQ_BK);
@@ -111,9 +111,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  const int arow = pi_row(m);                    // + 32*kb
-  const int trow = 8 * hh + (gi >> 2);           // + 32*kb + 16*half
-  const int tcol = 16 * (g & 1) + 4 * (gi & 3);  // + 32*c
+  const OperandOffsets o = operand_offsets(lane);
 
   for (int t = 0; t < n_tiles; ++t) {
     int k_row0, kpos, kn;
@@ -125,15 +123,13 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
     const lds_char* Vs = Ks + DQ_KBYTES;
     const bool full = (kn == DQ_BK) && (lo_last <= kpos) && (kpos + DQ_BK - 1 <= q_pos0);
 
-#pragma unroll 1
-    for (int kb = 0; kb < 2; ++kb) {
+    static_for<2>([&](auto kb_) {
+      constexpr int kb = decltype(kb_)::value;
       f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-      for (int t2 = 0; t2 < DQK / 16; ++t2)
-        s = mfma(lds_ld16(Ks, tile_off<DQK, DQ_BK>(32 * kb + arow, 2 * t2 + hh)), qf[t2], s);
+      for (int t2 = 0; t2 < DQK / 16; ++t2) s = mfma(op_b128<DQ_BK>(Ks, o, 32 * kb, t2), qf[t2], s);
 #pragma unroll
-      for (int t2 = 0; t2 < DV / 16; ++t2)
-        dp = mfma(lds_ld16(Vs, tile_off<DV, DQ_BK>(32 * kb + arow, 2 * t2 + hh)), df[t2], dp);
+      for (int t2 = 0; t2 < DV / 16; ++t2) dp = mfma(op_b128<DQ_BK>(Vs, o, 32 * kb, t2), df[t2], dp);
 
       float ds[16];
 #pragma unroll
@@ -147,23 +143,20 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
         }
         ds[e] = p * (dp[e] - Dq);
       }
-      const bf16x8 dsf0 = to_bf16x8(ds), dsf1 = to_bf16x8(ds + 8);
+      const bf16x8 dsf[2] = {to_bf16x8(ds), to_bf16x8(ds + 8)};
 
-      // dQ^T[c][q] += K^T[c][key] dS^T[key][q]; K^T fragments via LDS transpose reads,
-      // three column blocks at a time (the products of one group run while the next loads).
+      // dQ^T[c][q] += K^T[c][key] dS^T[key][q]; K^T fragments by LDS transpose reads, three
+      // column blocks per group; a group's products are issued before the next group loads.
+      bf16x8 f[2][3];
+      op_tr_x3<DQ_BK, 32 * kb, 0>(Ks, o, f[0]);
+      static_for<4>([&](auto g_) {
+        constexpr int gq = decltype(g_)::value, half = gq >> 1, c0 = 3 * (gq & 1);
 #pragma unroll
-      for (int half = 0; half < 2; ++half)
-#pragma unroll
-        for (int c0 = 0; c0 < DQK / 32; c0 += 3) {
-          bf16x8 f[3];
-#pragma unroll
-          for (int j = 0; j < 3; ++j)
-            f[j] = lds_tr_frag_async<DQK, DQ_BK>(Ks, 32 * kb + 16 * half + trow, 32 * (c0 + j) + tcol);
-          lds_wait(f[0], f[1], f[2]);
-#pragma unroll
-          for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[j], half ? dsf1 : dsf0, acc[c0 + j]);
-        }
-    }
+        for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], dsf[half], acc[c0 + j]);
+        if constexpr (gq + 1 < 4)
+          op_tr_x3<DQ_BK, 32 * kb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Ks, o, f[(gq + 1) & 1]);
+      });
+    });
   }
 
   if (q_valid) {
@@ -184,34 +177,45 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------ dK, dV (key-stationary)
-constexpr int KV_BQ = 64;                                 // query rows per stage
-constexpr int KV_QBYTES = KV_BQ * DQK * 2;                // 24 KB
-constexpr int KV_OBYTES = KV_BQ * DV * 2;                 // 16 KB
+// Eight waves share 128 keys as four pairs, one pair per SIMD, 32 keys per pair.  The two
+// waves of a pair split the work so that each fits in 256 registers (two waves per SIMD,
+// whose matrix and vector work then overlap):
+//   wave A: S = Q K^T, P = exp(S - LSE) (masked), dV^T += dO^T P
+//   wave B: dP = dO V^T, dS = P o (dP - D), dK^T += Q^T dS
+// P crosses from A to B through LDS (rounded to bf16, the value the dV product uses).  Per
+// 64-query tile: barrier, copy the tile two ahead, phase 1 (A: S and P, B: dP), barrier,
+// phase 2 (A: dV, B: dS and dK).
+constexpr int KV_BQ = 64;                                        // query rows per tile
+constexpr int KV_QBYTES = KV_BQ * DQK * 2;                       // 24 KB
+constexpr int KV_OBYTES = KV_BQ * DV * 2;                        // 16 KB
 constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_BQ * 4;  // + LSE2 and D
 constexpr int KV_NSTAGE = 3;
-// Vector-memory instructions one kv_issue adds per wave: 6 (Q) + 4 (dO) copies, plus one
-// vector copy on waves 0 and 1.  Waiting for vmcnt <= 10 therefore completes tile t while
+constexpr int KV_PBYTES = 4 * 2 * 2048;                          // P: 4 pairs x 2 sub-blocks x 32x32 bf16
+// Vector-memory instructions one kv_issue adds per wave (8 waves): 3 (Q) + 2 (dO) copies,
+// plus one vector copy on waves 0 and 1.  Waiting for vmcnt <= 5 completes tile t while
 // tile t+1 may stay in flight (waves 0 and 1 also finish one of t+1's copies).
-constexpr int KV_VMCNT_ONE_TILE = 10;
+constexpr int KV_VMCNT_ONE_TILE = 5;
 
 __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, const TileRanges qr, int t, int qoff,
                                          int ooff, int head, int wave, int lane) {
   int row0, pos0, n;
   tile_at(qr, t, KV_BQ, row0, pos0, n);
   lds_char* dst = smem + (t % KV_NSTAGE) * KV_STAGE;
-  dma_tile<DQK, KV_BQ>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff, a.H, wave);
-  dma_tile<DV, KV_BQ>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff, a.H, wave);
+  dma_tile<DQK, KV_BQ, 8>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff, a.H, wave);
+  dma_tile<DV, KV_BQ, 8>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff, a.H, wave);
   const int64_t li = (int64_t)head * a.nq + row0;
   if (wave == 0) dma_vec64(dst + KV_QBYTES + KV_OBYTES, a.lse2 + li, n, lane);
   if (wave == 1) dma_vec64(dst + KV_QBYTES + KV_OBYTES + KV_BQ * 4, a.Dvec + li, n, lane);
 }
 
-__global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem_raw[KV_NSTAGE * KV_STAGE];
+__global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem_raw[KV_NSTAGE * KV_STAGE + KV_PBYTES];
   lds_char* smem = (lds_char*)smem_raw;
+  lds_char* pbuf = smem + KV_NSTAGE * KV_STAGE;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int m = lane & 31, hh = lane >> 5, g = lane >> 4, gi = lane & 15;
+  const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV   role 1: dP, dS, dK
+  const int m = lane & 31, hh = lane >> 5;
   const int head = blockIdx.x % a.H;
   const Item it(a.items, blockIdx.x / a.H);
   const TileRanges qr = tile_ranges(it, KV_BQ);
@@ -219,15 +223,15 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(AttnArgs a) {
   if (n_tiles == 0) return;  // uniform over the workgroup
   const int k_row0 = it.row0, k_pos0 = it.pos0, k_n = it.n;
 
-  lds_clear<256>(smem, KV_NSTAGE * KV_STAGE, tid);
-  const int kj = wave * 32 + m;
+  lds_clear<512>(smem, KV_NSTAGE * KV_STAGE + KV_PBYTES, tid);
+  const int kj = pair * 32 + m;
   const bool k_valid = kj < k_n;
   const int pos_k = k_valid ? k_pos0 + kj : 0x7fffffff;
   int hi_k = k_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_k) + 1] : 0;
   // finish these loads here: left pending, the tile loop would wait for all copies in flight
   asm volatile("s_waitcnt vmcnt(0)" : "+v"(hi_k)::"memory");
-  const int kn_w = min(32, max(0, k_n - wave * 32));  // valid keys of this wave
-  const int wk_first = k_pos0 + wave * 32;
+  const int kn_w = min(32, max(0, k_n - pair * 32));  // valid keys of this pair
+  const int wk_first = k_pos0 + pair * 32;
   const int wk_last = wk_first + kn_w - 1;
   const int hi_first =
       __builtin_amdgcn_readfirstlane(kn_w > 0 ? a.cu[doc_of(a.cu, a.n_docs, wk_first) + 1] : 0);
@@ -236,45 +240,31 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int qoff = dma_lane_off<DQK>(a.H, head, wave, lane);
   const int ooff = dma_lane_off<DV>(a.H, head, wave, lane);
 
-  bf16x8 kf[DQK / 16], vf[DV / 16];
+  // role A keeps K^T fragments (B operand of S), role B keeps V^T fragments (B operand of dP)
+  constexpr int NF = DQK / 16;  // 12 (role B uses the first 8)
+  bf16x8 bf[NF];
   {
-    const uint16_t* kp = a.k + (krow * a.H + head) * DQK + 8 * hh;
-    const uint16_t* vp = a.v + (krow * a.H + head) * DV + 8 * hh;
-    u32x4 uk[DQK / 16], uv[DV / 16];
+    const uint16_t* src = role == 0 ? a.k + (krow * a.H + head) * DQK + 8 * hh : a.v + (krow * a.H + head) * DV + 8 * hh;
+    u32x4 u[NF];
 #pragma unroll
-    for (int t = 0; t < DQK / 16; ++t) uk[t] = u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int t = 0; t < DV / 16; ++t) uv[t] = u32x4{0u, 0u, 0u, 0u};
+    for (int t = 0; t < NF; ++t) u[t] = u32x4{0u, 0u, 0u, 0u};
     if (k_valid) {
-#pragma unroll
-      for (int t = 0; t < DQK / 16; ++t) uk[t] = ldg16_asm(kp + 16 * t);
-#pragma unroll
-      for (int t = 0; t < DV / 16; ++t) uv[t] = ldg16_asm(vp + 16 * t);
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-#pragma unroll
-    for (int t = 0; t < DQK / 16; ++t) {
-      asm volatile("" : "+v"(uk[t]));  // order every use after the wait above
-      kf[t] = __builtin_bit_cast(bf16x8, uk[t]);
+      ldg_x4(src, u[0], u[1], u[2], u[3]);
+      ldg_x4(src + 64, u[4], u[5], u[6], u[7]);
+      if (role == 0) ldg_x4(src + 128, u[8], u[9], u[10], u[11]);
     }
 #pragma unroll
-    for (int t = 0; t < DV / 16; ++t) {
-      asm volatile("" : "+v"(uv[t]));
-      vf[t] = __builtin_bit_cast(bf16x8, uv[t]);
-    }
+    for (int t = 0; t < NF; ++t) bf[t] = __builtin_bit_cast(bf16x8, u[t]);
   }
   __syncthreads();  // LDS cleared before the first copies land
   for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head, wave, lane);
 
-  f32x16 accK[DQK / 32], accV[DV / 32];
+  f32x16 acc[DQK / 32];  // role A: dV^T (first 4), role B: dK^T (6)
 #pragma unroll
-  for (int c = 0; c < DQK / 32; ++c) accK[c] = f32x16{};
-#pragma unroll
-  for (int d = 0; d < DV / 32; ++d) accV[d] = f32x16{};
+  for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  const int arow = pi_row(m);                    // + 32*sb
-  const int trow = 8 * hh + (gi >> 2);           // + 32*sb + 16*half
-  const int tcol = 16 * (g & 1) + 4 * (gi & 3);  // + 32*c
+  const OperandOffsets o = operand_offsets(lane);
+  const int poff = pair * 4096 + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
 
   for (int t = 0; t < n_tiles; ++t) {
     int q_row0, qpos, qn;
@@ -284,104 +274,130 @@ __global__ __launch_bounds__(256, 1) void bwd_dkdv_kernel(AttnArgs a) {
     else wait_dma();
     barrier_lds();
     if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head, wave, lane);
-    if (kn_w == 0) continue;  // wave-uniform; the barrier above is still reached
     const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
     const lds_char* Os = Qs + KV_QBYTES;
     const lds_char* vec_s = Qs + KV_QBYTES + KV_OBYTES;  // LSE2[64] then D[64]
+    const bool active = kn_w > 0;                       // uniform over the pair
 
-#pragma unroll 1
-    for (int sb = 0; sb < KV_BQ / 32; ++sb) {
-      const int qb = qpos + 32 * sb;
-      f32x16 s = f32x16{}, dp = f32x16{};
+    // ---------------- phase 1
+    // What crosses the barrier lives in one set of registers for both roles: role A keeps
+    // P of both sub-blocks (bf16, 16 dwords), role B keeps dP of both sub-blocks.
+    f32x16 carry[2];
+    if (active && role == 0) {
+      static_for<KV_BQ / 32>([&](auto sb_) {
+        constexpr int sb = decltype(sb_)::value;
+        const int qb = qpos + 32 * sb;
+        f32x16 s = f32x16{};
 #pragma unroll
-      for (int t2 = 0; t2 < DQK / 16; ++t2)
-        s = mfma(lds_ld16(Qs, tile_off<DQK, KV_BQ>(32 * sb + arow, 2 * t2 + hh)), kf[t2], s);
+        for (int t2 = 0; t2 < DQK / 16; ++t2) s = mfma(op_b128<KV_BQ>(Qs, o, 32 * sb, t2), bf[t2], s);
+        // this lane's query rows are 32*sb + 8*hh + {0..7, 16..23}
+        f32x4 l0, l1, l2, l3;
+        lds_x4_f32<128 * sb, 128 * sb + 16, 128 * sb + 64, 128 * sb + 80>(vec_s, 32 * hh, l0, l1, l2, l3);
+        const float lse_r[16] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3],
+                                 l2[0], l2[1], l2[2], l2[3], l3[0], l3[1], l3[2], l3[3]};
+        const bool full = (kn_w == 32) && (qn >= 32 * (sb + 1)) && (wk_last <= qb) && (qb + 31 < hi_first);
+        float p[16];
 #pragma unroll
-      for (int t2 = 0; t2 < DV / 16; ++t2)
-        dp = mfma(lds_ld16(Os, tile_off<DV, KV_BQ>(32 * sb + arow, 2 * t2 + hh)), vf[t2], dp);
-
-      const bool full = (kn_w == 32) && (qn >= 32 * (sb + 1)) && (wk_last <= qb) && (qb + 31 < hi_first);
-      // this lane's query rows are 32*sb + 8*hh + {0..7, 16..23}
-      f32x4 l0 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh)), l1 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh + 4));
-      f32x4 l2 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh + 16)), l3 = lds_f4_asm(vec_s, 4 * (32 * sb + 8 * hh + 20));
-      f32x4 d0 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh)), d1 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh + 4));
-      f32x4 d2 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh + 16));
-      f32x4 d3 = lds_f4_asm(vec_s, 4 * (KV_BQ + 32 * sb + 8 * hh + 20));
-      lds_wait4(l0, l1, l2, l3);
-      lds_wait4(d0, d1, d2, d3);
-      const float lse_r[16] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3],
-                               l2[0], l2[1], l2[2], l2[3], l3[0], l3[1], l3[2], l3[3]};
-      const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
-                             d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};
-      float p[16], ds[16];
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int qq = 32 * sb + 16 * (e >> 3) + 8 * hh + (e & 7);
-        float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
-        if (!full) {
-          const int pq = qpos + qq;
-          const bool vis = (qq < qn) && (pq >= pos_k) && (pq < hi_k);
-          pv = vis ? pv : 0.f;
+        for (int e = 0; e < 16; ++e) {
+          float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
+          if (!full) {
+            const int qq = 32 * sb + 16 * (e >> 3) + 8 * hh + (e & 7);
+            const int pq = qpos + qq;
+            const bool vis = (qq < qn) && (pq >= pos_k) && (pq < hi_k);
+            pv = vis ? pv : 0.f;
+          }
+          p[e] = pv;
         }
-        p[e] = pv;
-        ds[e] = pv * (dp[e] - D_r[e]);
+        const bf16x8 p0 = to_bf16x8(p), p1 = to_bf16x8(p + 8);
+        lds_st16<2048 * sb>(pbuf, poff, p0);
+        lds_st16<2048 * sb + 1024>(pbuf, poff, p1);
+        put_frag(carry[0], 8 * sb, p0);
+        put_frag(carry[0], 8 * sb + 4, p1);
+      });
+    } else if (active) {
+#pragma unroll
+      for (int sb = 0; sb < KV_BQ / 32; ++sb) {
+        carry[sb] = f32x16{};
+#pragma unroll
+        for (int t2 = 0; t2 < DV / 16; ++t2) carry[sb] = mfma(op_b128<KV_BQ>(Os, o, 32 * sb, t2), bf[t2], carry[sb]);
       }
-      const bf16x8 pf0 = to_bf16x8(p), pf1 = to_bf16x8(p + 8);
-      const bf16x8 sf0 = to_bf16x8(ds), sf1 = to_bf16x8(ds + 8);
+    }
+    barrier_lds();  // P of this tile is in LDS
 
+    // ---------------- phase 2
+    if (active && role == 0) {
+      // dV^T[dv][key] += dO^T[dv][q] P[q][key]; groups of four dO^T fragments, one per
+      // 16 query rows; a group's products are issued before the next group loads.
+      bf16x8 f[2][4];
+      op_tr_x4<KV_BQ, 0, 0>(Os, o, f[0]);
+      static_for<KV_BQ / 16>([&](auto g_) {
+        constexpr int gq = decltype(g_)::value;  // rows 16*gq .. 16*gq+15: sub-block gq/2, half gq%2
+        const bf16x8 pfr = get_frag(carry[0], 4 * gq);
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int r = 32 * sb + 16 * half + trow;
-        // dV^T[dv][key] += dO^T[dv][q] P[q][key]
-        {
-          bf16x8 f[4];
+        for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(f[gq & 1][d], pfr, acc[d]);
+        if constexpr (gq + 1 < KV_BQ / 16) op_tr_x4<KV_BQ, 16 * (gq + 1), 0>(Os, o, f[(gq + 1) & 1]);
+      });
+    } else if (active) {
+      static_for<KV_BQ / 32>([&](auto sb_) {
+        constexpr int sb = decltype(sb_)::value;
+        bf16x8 p0, p1;
+        lds_x2_bf16<2048 * sb, 2048 * sb + 1024>(pbuf, poff, p0, p1);
+        f32x4 d0, d1, d2, d3;
+        lds_x4_f32<256 + 128 * sb, 256 + 128 * sb + 16, 256 + 128 * sb + 64, 256 + 128 * sb + 80>(vec_s, 32 * hh, d0,
+                                                                                                  d1, d2, d3);
+        const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
+                               d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};
+        float ds[16];
 #pragma unroll
-          for (int d = 0; d < DV / 32; ++d) f[d] = lds_tr_frag_async<DV, KV_BQ>(Os, r, 32 * d + tcol);
-          lds_wait(f[0], f[1], f[2], f[3]);
-#pragma unroll
-          for (int d = 0; d < DV / 32; ++d) accV[d] = mfma(f[d], half ? pf1 : pf0, accV[d]);
+        for (int e = 0; e < 16; ++e) {
+          const float pv = (float)(e < 8 ? p0[e] : p1[e - 8]);
+          ds[e] = pv * (carry[sb][e] - D_r[e]);
         }
-        // dK^T[c][key] += Q^T[c][q] dS[q][key]
+        const bf16x8 sf[2] = {to_bf16x8(ds), to_bf16x8(ds + 8)};
+        // dK^T[c][key] += Q^T[c][q] dS[q][key]; groups of three Q^T column blocks
+        bf16x8 f[2][3];
+        op_tr_x3<KV_BQ, 32 * sb, 0>(Qs, o, f[0]);
+        static_for<4>([&](auto g_) {
+          constexpr int gq = decltype(g_)::value, half = gq >> 1, c0 = 3 * (gq & 1);
 #pragma unroll
-        for (int c0 = 0; c0 < DQK / 32; c0 += 3) {
-          bf16x8 f[3];
-#pragma unroll
-          for (int j = 0; j < 3; ++j) f[j] = lds_tr_frag_async<DQK, KV_BQ>(Qs, r, 32 * (c0 + j) + tcol);
-          lds_wait(f[0], f[1], f[2]);
-#pragma unroll
-          for (int j = 0; j < 3; ++j) accK[c0 + j] = mfma(f[j], half ? sf1 : sf0, accK[c0 + j]);
-        }
-      }
+          for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], sf[half], acc[c0 + j]);
+          if constexpr (gq + 1 < 4)
+            op_tr_x3<KV_BQ, 32 * sb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Qs, o, f[(gq + 1) & 1]);
+        });
+      });
     }
   }
 
   if (k_valid) {
-    float* dk = a.dk + (krow * a.H + head) * DQK + 4 * hh;
-    float* dv = a.dv + (krow * a.H + head) * DV + 4 * hh;
+    if (role == 0) {
+      float* dv = a.dv + (krow * a.H + head) * DV + 4 * hh;
 #pragma unroll
-    for (int c = 0; c < DQK / 32; ++c)
+      for (int d = 0; d < DV / 32; ++d)
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        f32x4* p = reinterpret_cast<f32x4*>(dk + 32 * c + 8 * rr);
-        f32x4 old = *p;
-        old[0] += a.scale * accK[c][4 * rr];
-        old[1] += a.scale * accK[c][4 * rr + 1];
-        old[2] += a.scale * accK[c][4 * rr + 2];
-        old[3] += a.scale * accK[c][4 * rr + 3];
-        *p = old;
-      }
+        for (int rr = 0; rr < 4; ++rr) {
+          f32x4* p = reinterpret_cast<f32x4*>(dv + 32 * d + 8 * rr);
+          f32x4 old = *p;
+          old[0] += acc[d][4 * rr];
+          old[1] += acc[d][4 * rr + 1];
+          old[2] += acc[d][4 * rr + 2];
+          old[3] += acc[d][4 * rr + 3];
+          *p = old;
+        }
+    } else {
+      float* dk = a.dk + (krow * a.H + head) * DQK + 4 * hh;
 #pragma unroll
-    for (int d = 0; d < DV / 32; ++d)
+      for (int c = 0; c < DQK / 32; ++c)
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        f32x4* p = reinterpret_cast<f32x4*>(dv + 32 * d + 8 * rr);
-        f32x4 old = *p;
-        old[0] += accV[d][4 * rr];
-        old[1] += accV[d][4 * rr + 1];
-        old[2] += accV[d][4 * rr + 2];
-        old[3] += accV[d][4 * rr + 3];
-        *p = old;
-      }
+        for (int rr = 0; rr < 4; ++rr) {
+          f32x4* p = reinterpret_cast<f32x4*>(dk + 32 * c + 8 * rr);
+          f32x4 old = *p;
+          old[0] += a.scale * acc[c][4 * rr];
+          old[1] += a.scale * acc[c][4 * rr + 1];
+          old[2] += a.scale * acc[c][4 * rr + 2];
+          old[3] += a.scale * acc[c][4 * rr + 3];
+          *p = old;
+        }
+    }
   }
 }
 
@@ -409,7 +425,7 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
     b.items = kitems;
     b.n_items = n_kitems;
     tok = prof_begin("bwd_dkdv", stream);
-    hipLaunchKernelGGL(bwd_dkdv_kernel, dim3(n_kitems * a.H), dim3(256), 0, stream, b);
+    hipLaunchKernelGGL(bwd_dkdv_kernel, dim3(n_kitems * a.H), dim3(512), 0, stream, b);
     prof_end(tok, stream);
     e = hipGetLastError();
   }

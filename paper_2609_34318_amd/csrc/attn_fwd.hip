@@ -39,7 +39,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
   lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int m = lane & 31, hh = lane >> 5, g = lane >> 4, gi = lane & 15;
+  const int m = lane & 31, hh = lane >> 5;
   const int head = blockIdx.x % a.H;
   const Item it(a.items, blockIdx.x / a.H);
   const int q_row0 = it.row0, q_pos0 = it.pos0, q_n = it.n;
@@ -76,9 +76,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
   for (int d = 0; d < DV / 32; ++d) acc[d] = f32x16{};
   float m_run = NEG_BIG, l_run = 0.f;
 
-  const int krow = pi_row(m);                    // + 32*kb
-  const int vrow = 8 * hh + (gi >> 2);           // + 16*st
-  const int vcol = 16 * (g & 1) + 4 * (gi & 3);  // + 32*d
+  const OperandOffsets o = operand_offsets(lane);
 
   for (int t = 0; t < n_tiles; ++t) {
     int k_row0, kpos, kn;
@@ -95,7 +93,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
       s[kb] = f32x16{};
 #pragma unroll
       for (int t2 = 0; t2 < DQK / 16; ++t2)
-        s[kb] = mfma(lds_ld16(Ks, tile_off<DQK, FWD_BK>(32 * kb + krow, 2 * t2 + hh)), qf[t2], s[kb]);
+        s[kb] = mfma(op_b128<FWD_BK>(Ks, o, 32 * kb, t2), qf[t2], s[kb]);
     }
 
     const bool full = (kn == FWD_BK) && (lo_last <= kpos) && (kpos + FWD_BK - 1 <= q_pos0);
@@ -141,23 +139,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
       pf[2 * kb + 1] = to_bf16x8(p + 8);
     }
 
-    // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads,
-    // the reads for step st+1 in flight while step st's products run.
+    // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads.  The
+    // products of key step st are issued before the fragments of step st+1 load.
     bf16x8 vf[2][DV / 32];
+    op_tr_x4<FWD_BK, 0, 0>(Vs, o, vf[0]);
+    static_for<4>([&](auto st_) {
+      constexpr int st = decltype(st_)::value;
 #pragma unroll
-    for (int d = 0; d < DV / 32; ++d) vf[0][d] = lds_tr_frag_async<DV, FWD_BK>(Vs, vrow, 32 * d + vcol);
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      bf16x8* cur = vf[st & 1];
-      lds_wait(cur[0], cur[1], cur[2], cur[3]);
-      if (st + 1 < 4) {
-#pragma unroll
-        for (int d = 0; d < DV / 32; ++d)
-          vf[(st + 1) & 1][d] = lds_tr_frag_async<DV, FWD_BK>(Vs, 16 * (st + 1) + vrow, 32 * d + vcol);
-      }
-#pragma unroll
-      for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(cur[d], pf[st], acc[d]);
-    }
+      for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(vf[st & 1][d], pf[st], acc[d]);
+      if constexpr (st + 1 < 4) op_tr_x4<FWD_BK, 16 * (st + 1), 0>(Vs, o, vf[(st + 1) & 1]);
+    });
   }
 
   const float l_tot = xhalf_sum(l_run);

@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 namespace hydra {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -35,11 +37,6 @@ constexpr int MAX_RANGES = 4;
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 constexpr float NEG_BIG = -1.0e30f;  // finite running-max floor: keeps exp2 arguments NaN-free
-
-// LDS row pitches (bf16 elements): 16 bytes of padding per row spreads consecutive rows
-// over different banks for 16-byte reads.
-constexpr int PITCH_QK = DQK + 8;  // 400 bytes
-constexpr int PITCH_V = DV + 8;    // 272 bytes
 
 __device__ __forceinline__ int pi_row(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
@@ -59,21 +56,6 @@ __device__ __forceinline__ float xhalf_sum(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__device__ __forceinline__ bf16x8 lds_read8(const __bf16* p) {
-  return *reinterpret_cast<const bf16x8*>(p);
-}
-
-// Two transpose reads: rows r0..r0+3 and r0+4..r0+7 (see the header comment).
-__device__ __forceinline__ bf16x8 lds_read8_tr(const __bf16* p0, const __bf16* p1) {
-  i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(
-      (lds_char*)(p0)));
-  i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(
-      (lds_char*)(p1)));
-  typedef short i16x8 __attribute__((ext_vector_type(8)));
-  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  return __builtin_bit_cast(bf16x8, v);
-}
-
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   __bf16 x = (__bf16)a, y = (__bf16)b;
   return uint32_t(__builtin_bit_cast(uint16_t, x)) | (uint32_t(__builtin_bit_cast(uint16_t, y)) << 16);
@@ -89,17 +71,22 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const float* v) {
   return __builtin_bit_cast(bf16x8, u);
 }
 
-__device__ __forceinline__ u32x4 ldg16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
-
-// 16-byte global load as inline assembly, for operands loaded once before a tile loop whose
-// copies are waited for with partial vmcnt counts: the compiler's wait insertion would
-// otherwise keep such registers "possibly pending" across the loop back edge and wait for
-// every copy in flight before each use.  Complete them with wait_vmem_all() before use.
-__device__ __forceinline__ u32x4 ldg16_asm(const void* p) {
-  u32x4 v;
-  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
-  return v;
+// A bf16 fragment stored in / read from four fp32 register slots of an accumulator-shaped
+// value (register reuse across roles; no data conversion).
+__device__ __forceinline__ void put_frag(f32x16& r, int at, bf16x8 v) {
+  const u32x4 u = __builtin_bit_cast(u32x4, v);
+  r[at] = __uint_as_float(u[0]);
+  r[at + 1] = __uint_as_float(u[1]);
+  r[at + 2] = __uint_as_float(u[2]);
+  r[at + 3] = __uint_as_float(u[3]);
 }
+__device__ __forceinline__ bf16x8 get_frag(const f32x16& r, int at) {
+  u32x4 u = {__float_as_uint(r[at]), __float_as_uint(r[at + 1]), __float_as_uint(r[at + 2]),
+             __float_as_uint(r[at + 3])};
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+__device__ __forceinline__ u32x4 ldg16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
 // Largest d with cu[d] <= pos (cu has n_docs + 1 entries, pos inside the window).
 __device__ __forceinline__ int doc_of(const int* __restrict__ cu, int n_docs, int pos) {
@@ -112,88 +99,197 @@ __device__ __forceinline__ int doc_of(const int* __restrict__ cu, int n_docs, in
 }
 
 // ------------------------------------------------------------------ swizzled LDS tiles
-// Tiles are stored unpadded.  d = 128 tiles: ROWS rows of 256 B.  d = 192 tiles: three
-// column blocks of 64 elements, each ROWS rows of 128 B, so that one 1 KB direct-to-LDS
-// instruction always covers whole rows (4 or 8).  Within a row the 16-byte chunk c lives at
-// chunk c ^ swz(r); the XOR spreads both the 16-byte operand reads (16 rows, one chunk) and
-// the transpose reads (4 rows x 4 chunks) over all 64 LDS banks.
-__device__ __forceinline__ int swz256(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
-__device__ __forceinline__ int swz128(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
+// A tile of ROWS rows and DIM (128 or 192) bf16 columns is stored as DIM/64 column blocks of
+// 64 elements; each block is ROWS rows of 128 bytes, unpadded, so that one 1 KB direct-to-LDS
+// instruction covers 8 whole rows.  Within a row the 16-byte chunk c (0..7) lives at chunk
+// c ^ swz(r), which spreads both the 16-byte operand reads (16 rows, one chunk) and the
+// transpose reads (4 rows x 4 chunks) over all 64 LDS banks.  swz(r) only looks at bits
+// 1..3 of r, so every read below is a per-lane constant plus a compile-time offset.
+__device__ __forceinline__ int swz(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
 
-// Byte offset of logical 16-byte chunk `c` of row `r` in a tile of ROWS rows.
-template <int DIM, int ROWS> __device__ __forceinline__ int tile_off(int r, int c);
-template <> __device__ __forceinline__ int tile_off<128, 64>(int r, int c) { return r * 256 + ((c ^ swz256(r)) << 4); }
-template <> __device__ __forceinline__ int tile_off<128, 32>(int r, int c) { return r * 256 + ((c ^ swz256(r)) << 4); }
-template <> __device__ __forceinline__ int tile_off<192, 64>(int r, int c) {
-  return (c >> 3) * (64 * 128) + r * 128 + (((c & 7) ^ swz128(r)) << 4);
+template <int ROWS> constexpr int block_bytes() { return ROWS * 128; }
+
+// Byte offset of logical 16-byte chunk `c` (0 .. DIM/8-1) of row `r`.
+template <int ROWS> __device__ __forceinline__ int tile_off(int r, int c) {
+  return (c >> 3) * block_bytes<ROWS>() + r * 128 + (((c & 7) ^ swz(r)) << 4);
 }
-template <> __device__ __forceinline__ int tile_off<192, 32>(int r, int c) {
-  return (c >> 3) * (32 * 128) + r * 128 + (((c & 7) ^ swz128(r)) << 4);
+
+// Lane-constant parts of the operand reads of a 32x32x16 MFMA from such tiles.
+//   b128[j]: 16-byte read of row pi(m), chunk 2j + h within a column block (k-step t uses
+//            j = t & 3, block t >> 2)
+//   tr[v][k]: transpose read at row (v ? 4 : 0) + 8h + i/4, column 32*cb + 16*(g&1) + 4*(i&3)
+//            with k = cb & 1 (block cb >> 1)
+// Callers add row_block*128 (row_block a multiple of 16) and block*block_bytes as immediates.
+struct OperandOffsets {
+  int b128[4];
+  int tr[2][2];
+};
+
+__device__ __forceinline__ OperandOffsets operand_offsets(int lane) {
+  const int m = lane & 31, h = lane >> 5, g = lane >> 4, gi = lane & 15;
+  OperandOffsets o;
+  const int ra = pi_row(m);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) o.b128[j] = ra * 128 + (((2 * j + h) ^ swz(ra)) << 4);
+  const int rt = 8 * h + (gi >> 2);
+  const int cl = 2 * (g & 1) + ((gi & 3) >> 1);  // chunk within 4, plus the 8-byte half below
+  const int w = (gi & 1) << 3;
+#pragma unroll
+  for (int v = 0; v < 2; ++v)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int r = rt + 4 * v;
+      o.tr[v][k] = r * 128 + (((4 * k + cl) ^ swz(r)) << 4) + w;
+    }
+  return o;
 }
 
 __device__ __forceinline__ bf16x8 lds_ld16(const lds_char* base, int off) {
   return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(base + off);
 }
 
-__device__ __forceinline__ i16x4 lds_tr8(const lds_char* base, int off) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(base + off));
+// k-step t of a b128 operand at rows row_block + pi(m) of a ROWS-row tile.
+template <int ROWS>
+__device__ __forceinline__ bf16x8 op_b128(const lds_char* tile, const OperandOffsets& o, int row_block, int t) {
+  return lds_ld16(tile, o.b128[t & 3] + (t >> 2) * block_bytes<ROWS>() + row_block * 128);
 }
 
-// Transposed operand fragment: each lane points at row `row` (and row + 4) and element
-// column `col`; the transpose read hands lane i of each 16-lane group one column of the
-// 4 x 16 block its group addressed (see the header comment).
-template <int DIM, int ROWS>
-__device__ __forceinline__ bf16x8 lds_tr_frag(const lds_char* base, int row, int col) {
-  const int c = col >> 3, w = (col & 7) << 1;
-  i16x4 lo = lds_tr8(base, tile_off<DIM, ROWS>(row, c) + w);
-  i16x4 hi = lds_tr8(base, tile_off<DIM, ROWS>(row + 4, c) + w);
+// ------------------------------------------------------------------ LDS reads as inline assembly
+// The compiler's wait insertion treats the transpose-read builtin, and any LDS access after a
+// direct-to-LDS copy, as a possible alias of every copy still in flight (including the
+// prefetch into another stage) and waits for all of them first.  The reads below are
+// therefore inline assembly.  Each group of reads and its s_waitcnt are ONE asm statement
+// with early-clobber outputs: a read's destination registers are written when the data
+// arrives, so no instruction may touch them (not even a register copy the allocator might
+// insert) until the wait.  Offsets that are compile-time constants travel in the
+// instruction's offset field.
+
+template <int N> struct IntC { static constexpr int value = N; };
+
+// Calls f(IntC<0>{}) .. f(IntC<N-1>{}) (compile-time loop index).
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(IntC<I>{}), ...);
+}
+template <int N, class F> __device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const lds_char* p) { return (uint32_t)(uintptr_t)p; }
+
+__device__ __forceinline__ bf16x8 join(i16x4 lo, i16x4 hi) {
   typedef short i16x8 __attribute__((ext_vector_type(8)));
   i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// The same transpose read issued as inline assembly.  The compiler's wait insertion treats
-// the builtin as a possible alias of every direct-to-LDS copy still in flight (including
-// the prefetch into the other stage) and waits for all of them first; the asm form is not
-// tracked by that pass, so the caller must wait for it explicitly with lds_wait(), which
-// also ties the fragments to the wait so their consumers cannot move above it.
-__device__ __forceinline__ i16x4 lds_tr8_asm(const lds_char* base, int off) {
-  i16x4 v;
-  const uint32_t addr = (uint32_t)(uintptr_t)(base + off);
-  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-  return v;
+// Transposed operand fragments for column blocks CB0 .. CB0+N-1 (N = 3 or 4) of rows
+// ROWB .. ROWB+15 of a ROWS-row tile (lane pattern of OperandOffsets::tr), read and waited for.
+template <int ROWS, int ROWB, int CB0, int N> struct TrGroup {
+  static constexpr int imm(int n) { return ((CB0 + n) >> 1) * block_bytes<ROWS>() + ROWB * 128; }
+  static constexpr int par(int n) { return (CB0 + n) & 1; }
+};
+
+template <int ROWS, int ROWB, int CB0>
+__device__ __forceinline__ void op_tr_x4(const lds_char* tile, const OperandOffsets& o, bf16x8 (&f)[4]) {
+  using G = TrGroup<ROWS, ROWB, CB0, 4>;
+  const uint32_t b = lds_addr(tile);
+  i16x4 r0, r1, r2, r3, r4, r5, r6, r7;
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
+      "ds_read_b64_tr_b16 %1, %9 offset:%17\n\t"
+      "ds_read_b64_tr_b16 %2, %10 offset:%18\n\t"
+      "ds_read_b64_tr_b16 %3, %11 offset:%19\n\t"
+      "ds_read_b64_tr_b16 %4, %12 offset:%20\n\t"
+      "ds_read_b64_tr_b16 %5, %13 offset:%21\n\t"
+      "ds_read_b64_tr_b16 %6, %14 offset:%22\n\t"
+      "ds_read_b64_tr_b16 %7, %15 offset:%23\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3), "=&v"(r4), "=&v"(r5), "=&v"(r6), "=&v"(r7)
+      : "v"(b + o.tr[0][G::par(0)]), "v"(b + o.tr[1][G::par(0)]), "v"(b + o.tr[0][G::par(1)]),
+        "v"(b + o.tr[1][G::par(1)]), "v"(b + o.tr[0][G::par(2)]), "v"(b + o.tr[1][G::par(2)]),
+        "v"(b + o.tr[0][G::par(3)]), "v"(b + o.tr[1][G::par(3)]), "i"(G::imm(0)), "i"(G::imm(0)),
+        "i"(G::imm(1)), "i"(G::imm(1)), "i"(G::imm(2)), "i"(G::imm(2)), "i"(G::imm(3)), "i"(G::imm(3))
+      : "memory");
+  f[0] = join(r0, r1);
+  f[1] = join(r2, r3);
+  f[2] = join(r4, r5);
+  f[3] = join(r6, r7);
 }
 
-template <int DIM, int ROWS>
-__device__ __forceinline__ bf16x8 lds_tr_frag_async(const lds_char* base, int row, int col) {
-  const int c = col >> 3, w = (col & 7) << 1;
-  i16x4 lo = lds_tr8_asm(base, tile_off<DIM, ROWS>(row, c) + w);
-  i16x4 hi = lds_tr8_asm(base, tile_off<DIM, ROWS>(row + 4, c) + w);
-  typedef short i16x8 __attribute__((ext_vector_type(8)));
-  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  return __builtin_bit_cast(bf16x8, v);
+template <int ROWS, int ROWB, int CB0>
+__device__ __forceinline__ void op_tr_x3(const lds_char* tile, const OperandOffsets& o, bf16x8 (&f)[3]) {
+  using G = TrGroup<ROWS, ROWB, CB0, 3>;
+  const uint32_t b = lds_addr(tile);
+  i16x4 r0, r1, r2, r3, r4, r5;
+  asm volatile(
+      "ds_read_b64_tr_b16 %0, %6 offset:%12\n\t"
+      "ds_read_b64_tr_b16 %1, %7 offset:%13\n\t"
+      "ds_read_b64_tr_b16 %2, %8 offset:%14\n\t"
+      "ds_read_b64_tr_b16 %3, %9 offset:%15\n\t"
+      "ds_read_b64_tr_b16 %4, %10 offset:%16\n\t"
+      "ds_read_b64_tr_b16 %5, %11 offset:%17\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3), "=&v"(r4), "=&v"(r5)
+      : "v"(b + o.tr[0][G::par(0)]), "v"(b + o.tr[1][G::par(0)]), "v"(b + o.tr[0][G::par(1)]),
+        "v"(b + o.tr[1][G::par(1)]), "v"(b + o.tr[0][G::par(2)]), "v"(b + o.tr[1][G::par(2)]),
+        "i"(G::imm(0)), "i"(G::imm(0)), "i"(G::imm(1)), "i"(G::imm(1)), "i"(G::imm(2)), "i"(G::imm(2))
+      : "memory");
+  f[0] = join(r0, r1);
+  f[1] = join(r2, r3);
+  f[2] = join(r4, r5);
 }
 
-// Four floats from LDS as inline assembly (same reason as lds_tr8_asm); wait with lds_wait4.
-__device__ __forceinline__ f32x4 lds_f4_asm(const lds_char* base, int off) {
-  f32x4 v;
-  const uint32_t addr = (uint32_t)(uintptr_t)(base + off);
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-  return v;
-}
-__device__ __forceinline__ void lds_wait4(f32x4& a, f32x4& b, f32x4& c, f32x4& d) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d)::"memory");
+// Four 16-byte LDS reads at base + lane_off + I0..I3, waited for.
+template <int I0, int I1, int I2, int I3>
+__device__ __forceinline__ void lds_x4_f32(const lds_char* base, int lane_off, f32x4& a, f32x4& b, f32x4& c,
+                                           f32x4& d) {
+  const uint32_t ad = lds_addr(base) + lane_off;
+  asm volatile(
+      "ds_read_b128 %0, %4 offset:%5\n\t"
+      "ds_read_b128 %1, %4 offset:%6\n\t"
+      "ds_read_b128 %2, %4 offset:%7\n\t"
+      "ds_read_b128 %3, %4 offset:%8\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(a), "=&v"(b), "=&v"(c), "=&v"(d)
+      : "v"(ad), "i"(I0), "i"(I1), "i"(I2), "i"(I3)
+      : "memory");
 }
 
-// Waits for every outstanding LDS read and marks the fragments as produced here.
-__device__ __forceinline__ void lds_wait(bf16x8& a, bf16x8& b, bf16x8& c, bf16x8& d) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d)::"memory");
+// Two 16-byte LDS reads at base + lane_off + I0, I1, waited for.
+template <int I0, int I1>
+__device__ __forceinline__ void lds_x2_bf16(const lds_char* base, int lane_off, bf16x8& a, bf16x8& b) {
+  const uint32_t ad = lds_addr(base) + lane_off;
+  asm volatile(
+      "ds_read_b128 %0, %2 offset:%3\n\t"
+      "ds_read_b128 %1, %2 offset:%4\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(a), "=&v"(b)
+      : "v"(ad), "i"(I0), "i"(I1)
+      : "memory");
 }
-__device__ __forceinline__ void lds_wait(bf16x8& a, bf16x8& b) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b)::"memory");
+
+// 16-byte LDS store of an operand fragment (a hand-off buffer the compiler would otherwise
+// order behind the copies in flight).
+template <int I0>
+__device__ __forceinline__ void lds_st16(lds_char* base, int lane_off, bf16x8 v) {
+  const uint32_t ad = lds_addr(base) + lane_off;
+  asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(ad), "v"(v), "i"(I0) : "memory");
 }
-__device__ __forceinline__ void lds_wait(bf16x8& a, bf16x8& b, bf16x8& c) {
-  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(b), "+v"(c)::"memory");
+
+// N (<= 12) 16-byte global loads from p + 16*t elements... issued and completed in one
+// statement, for operands loaded once before a tile loop (left pending, the compiler would
+// wait for every copy in flight before their uses inside the loop).
+__device__ __forceinline__ void ldg_x4(const uint16_t* p, u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
+  asm volatile(
+      "global_load_dwordx4 %0, %4, off\n\t"
+      "global_load_dwordx4 %1, %4, off offset:32\n\t"
+      "global_load_dwordx4 %2, %4, off offset:64\n\t"
+      "global_load_dwordx4 %3, %4, off offset:96\n\t"
+      "s_waitcnt vmcnt(0)"
+      : "=&v"(a), "=&v"(b), "=&v"(c), "=&v"(d)
+      : "v"(p)
+      : "memory");
 }
 
 // ------------------------------------------------------------------ direct global -> LDS copies
@@ -208,20 +304,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* g, i
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, valid * H * dim * 2, 0x00020000);
 }
 
-// Per-lane byte offset (tile-independent) for dma_tile with 4 waves.  Lane L of wave w writes
-// bytes [16L, 16L+16) of each 1 KB instruction, which holds rows 4j..4j+3 (d = 128) or
-// 8j..8j+7 of one column block (d = 192), j = w + 4i; it fetches the logical chunk the
-// swizzle places there.
-template <int DIM> __device__ __forceinline__ int dma_lane_off(int H, int head, int wave, int lane);
-template <> __device__ __forceinline__ int dma_lane_off<128>(int H, int head, int wave, int lane) {
-  const int q = lane >> 4;
-  const int lc = (lane & 15) ^ ((q << 2) | (wave & 3));
-  return (((4 * wave + q) * H + head) * 128 + lc * 8) * 2;
-}
-template <> __device__ __forceinline__ int dma_lane_off<192>(int H, int head, int wave, int lane) {
+// Per-lane byte offset (tile-independent) for dma_tile with NW = 4 or 8 waves.  Lane L of
+// wave w writes bytes [16L, 16L+16) of each 1 KB instruction, which holds rows 8j..8j+7 of
+// one column block, j = w + NW*i; it fetches the logical chunk the swizzle places there
+// (rows 8j + L/8 have bits 1..3 = (L/8 >> 1) and (j & 1) == (w & 1) for every i).
+template <int DIM> __device__ __forceinline__ int dma_lane_off(int H, int head, int wave, int lane) {
   const int q = lane >> 3;
   const int lc = (lane & 7) ^ ((((q >> 1) & 1) << 2) | ((wave & 1) << 1) | (q >> 2));
-  return (((8 * wave + q) * H + head) * 192 + lc * 8) * 2;
+  return (((8 * wave + q) * H + head) * DIM + lc * 8) * 2;
 }
 
 // voff + inc, computed where it is used: the compiler would otherwise hoist one VGPR per
@@ -233,27 +323,20 @@ __device__ __forceinline__ int add_here(int voff, int inc) {
   return o;
 }
 
-template <int DIM, int ROWS>
+template <int DIM, int ROWS, int NW = 4>
 __device__ __forceinline__ void dma_tile(lds_char* lds, __amdgpu_buffer_rsrc_t rs, int voff, int H, int wave) {
   typedef __attribute__((address_space(3))) void lds_void;
-  if constexpr (DIM == 128) {
-    constexpr int NINS = ROWS / 4;
-    static_assert(NINS % 4 == 0, "tile must split evenly over 4 waves");
+  constexpr int NINS = ROWS / 8;  // per column block
+  static_assert(NINS % NW == 0, "tile must split evenly over the waves");
 #pragma unroll
-    for (int i = 0; i < NINS / 4; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + (wave + 4 * i) * 1024), 16,
-                                               i == 0 ? voff : add_here(voff, 16 * i * H * 256), 0, 0, 0);
-  } else {
-    constexpr int NINS = ROWS / 8;  // per column block
-    static_assert(NINS % 4 == 0, "tile must split evenly over 4 waves");
+  for (int b = 0; b < DIM / 64; ++b)
 #pragma unroll
-    for (int b = 0; b < 3; ++b)
-#pragma unroll
-      for (int i = 0; i < NINS / 4; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + b * ROWS * 128 + (wave + 4 * i) * 1024), 16,
-                                                 (b == 0 && i == 0) ? voff : add_here(voff, 32 * i * H * 384 + b * 128),
-                                                 0, 0, 0);
-  }
+    for (int i = 0; i < NINS / NW; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + b * block_bytes<ROWS>() + (wave + NW * i) * 1024),
+                                               16,
+                                               (b == 0 && i == 0) ? voff
+                                                                  : add_here(voff, 8 * NW * i * H * DIM * 2 + b * 128),
+                                               0, 0, 0);
 }
 
 // 64 consecutive floats (one per lane) into LDS; entries past `valid` are out of range.
@@ -337,24 +420,6 @@ __device__ __forceinline__ void tile_at(const TileRanges R, int t, int B, int& r
   row0 = rr + off;
   pos0 = pp + off;
   n = min(B, cc - off);
-}
-
-// Stage `rows` rows (of at most 32*n_sub) of a [token][head][dim] bf16 tensor into an LDS
-// tile with the given pitch; rows beyond `valid` are zero-filled.
-template <int DIM, int PITCH, int ROWS, int THREADS>
-__device__ __forceinline__ void stage_rows(__bf16* lds, const uint16_t* __restrict__ g, int64_t row0,
-                                           int valid, int H, int head, int tid) {
-  constexpr int CH = DIM / 8;  // 16-byte chunks per row
-  constexpr int TOTAL = ROWS * CH;
-  static_assert(TOTAL % THREADS == 0, "tile must split evenly over the workgroup");
-#pragma unroll
-  for (int i = 0; i < TOTAL / THREADS; ++i) {
-    const int c = tid + i * THREADS;
-    const int r = c / CH, col = (c % CH) * 8;
-    u32x4 val = {0u, 0u, 0u, 0u};
-    if (r < valid) val = ldg16(g + ((row0 + r) * H + head) * (int64_t)DIM + col);
-    *reinterpret_cast<u32x4*>(lds + r * PITCH + col) = val;
-  }
 }
 
 struct AttnArgs {

@@ -64,7 +64,8 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * DQ_STAGE];
   lds_char* smem = (lds_char*)smem_raw;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, known to the compiler
   const int m = lane & 31, hh = lane >> 5;
   const int head = blockIdx.x % a.H;
   const Item it(a.items, blockIdx.x / a.H);
@@ -132,16 +133,21 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
       for (int t2 = 0; t2 < DV / 16; ++t2) dp = mfma(op_b128<DQ_BK>(Vs, o, 32 * kb, t2), df[t2], dp);
 
       float ds[16];
+      if (full) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse2));
-        if (!full) {
-          const int key = kb * 32 + 16 * (e >> 3) + 8 * hh + (e & 7);
-          const int kp = kpos + key;
-          const bool vis = (key < kn) && (kp <= pos_q) && (kp >= lo_q);
-          p = vis ? p : 0.f;
+        for (int e = 0; e < 16; ++e) ds[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse2)) * (dp[e] - Dq);
+      } else {
+        // key kpos + key(e) is visible iff lo_q <= it <= pos_q and key(e) < kn, i.e. iff
+        // 0 <= base + c(e) < lim with base = kpos - lo_q + 32*kb + 8*hh; masked entries get
+        // exp2(-inf) = 0
+        const int base = kpos - lo_q + 32 * kb + 8 * hh;
+        const int lim = q_valid ? max(0, min(pos_q + 1, kpos + kn) - lo_q) : 0;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = base + 16 * (e >> 3) + (e & 7);
+          const bool vis = (unsigned)r < (unsigned)lim;
+          ds[e] = __builtin_amdgcn_exp2f(vis ? __builtin_fmaf(s[e], sl2, -lse2) : -INFINITY) * (dp[e] - Dq);
         }
-        ds[e] = p * (dp[e] - Dq);
       }
       const bf16x8 dsf[2] = {to_bf16x8(ds), to_bf16x8(ds + 8)};
 
@@ -214,6 +220,10 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   lds_char* pbuf = smem + KV_NSTAGE * KV_STAGE;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // The same value, known to the compiler to be wave-uniform: the copy issue selects its
+  // sources with it (a per-lane select there turns each copy into a waterfall loop), while
+  // the role branches keep the per-lane form, under which both roles fit their registers.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV   role 1: dP, dS, dK
   const int m = lane & 31, hh = lane >> 5;
   const int head = blockIdx.x % a.H;
@@ -257,7 +267,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
     for (int t = 0; t < NF; ++t) bf[t] = __builtin_bit_cast(bf16x8, u[t]);
   }
   __syncthreads();  // LDS cleared before the first copies land
-  for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head, wave, lane);
+  for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head, wave_u, lane);
 
   f32x16 acc[DQK / 32];  // role A: dV^T (first 4), role B: dK^T (6)
 #pragma unroll
@@ -273,7 +283,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
     if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
     else wait_dma();
     barrier_lds();
-    if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head, wave, lane);
+    if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head, wave_u, lane);
     const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
     const lds_char* Os = Qs + KV_QBYTES;
     const lds_char* vec_s = Qs + KV_QBYTES + KV_OBYTES;  // LSE2[64] then D[64]
@@ -297,16 +307,20 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
                                  l2[0], l2[1], l2[2], l2[3], l3[0], l3[1], l3[2], l3[3]};
         const bool full = (kn_w == 32) && (qn >= 32 * (sb + 1)) && (wk_last <= qb) && (qb + 31 < hi_first);
         float p[16];
+        if (full) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
-          if (!full) {
-            const int qq = 32 * sb + 16 * (e >> 3) + 8 * hh + (e & 7);
-            const int pq = qpos + qq;
-            const bool vis = (qq < qn) && (pq >= pos_k) && (pq < hi_k);
-            pv = vis ? pv : 0.f;
+          for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
+        } else {
+          // query row qq = base + c(e) is visible iff lo <= base + c(e) < lim, where base is
+          // this lane's first row relative to its key position; masked entries get exp2(-inf)
+          const int base = qpos - pos_k + 32 * sb + 8 * hh;
+          const int lim = k_valid ? max(0, min(qpos + qn, hi_k) - pos_k) : 0;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int r = base + 16 * (e >> 3) + (e & 7);
+            const bool vis = (unsigned)r < (unsigned)lim;
+            p[e] = __builtin_amdgcn_exp2f(vis ? __builtin_fmaf(s[e], sl2, -lse_r[e]) : -INFINITY);
           }
-          p[e] = pv;
         }
         const bf16x8 p0 = to_bf16x8(p), p1 = to_bf16x8(p + 8);
         lds_st16<2048 * sb>(pbuf, poff, p0);

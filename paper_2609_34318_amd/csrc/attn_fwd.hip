@@ -38,7 +38,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
   __shared__ __attribute__((aligned(1024))) char smem_raw[2 * FWD_STAGE];
   lds_char* smem = (lds_char*)smem_raw;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, known to the compiler
   const int m = lane & 31, hh = lane >> 5;
   const int head = blockIdx.x % a.H;
   const Item it(a.items, blockIdx.x / a.H);

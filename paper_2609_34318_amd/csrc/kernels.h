@@ -44,7 +44,7 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float fmax2(float a, float b) { return a > b ? a : b; }
+__device__ __forceinline__ float fmax2(float a, float b) { return __builtin_fmaxf(a, b); }
 
 // Value held by the lane 32 positions away (m stays, h flips) and the max / sum with it.
 __device__ __forceinline__ float xhalf_max(float v) {
@@ -61,14 +61,11 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return uint32_t(__builtin_bit_cast(uint16_t, x)) | (uint32_t(__builtin_bit_cast(uint16_t, y)) << 16);
 }
 
-// Eight fp32 values -> one bf16 operand fragment (round to nearest even).
+// Eight fp32 values -> one bf16 operand fragment (round to nearest even, v_cvt_pk_bf16_f32).
 __device__ __forceinline__ bf16x8 to_bf16x8(const float* v) {
-  u32x4 u;
-  u[0] = pack_bf16x2(v[0], v[1]);
-  u[1] = pack_bf16x2(v[2], v[3]);
-  u[2] = pack_bf16x2(v[4], v[5]);
-  u[3] = pack_bf16x2(v[6], v[7]);
-  return __builtin_bit_cast(bf16x8, u);
+  typedef float f32x8 __attribute__((ext_vector_type(8)));
+  const f32x8 x = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
+  return __builtin_convertvector(x, bf16x8);
 }
 
 // A bf16 fragment stored in / read from four fp32 register slots of an accumulator-shaped

@@ -50,18 +50,21 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict
 constexpr int DQ_BK = 64;
 constexpr int DQ_KBYTES = DQ_BK * DQK * 2;            // 24 KB
 constexpr int DQ_STAGE = DQ_KBYTES + DQ_BK * DV * 2;  // 40 KB
+constexpr int DQ_NSTAGE = 3;
+constexpr int DQ_WAVES = 8;                           // 256 query rows per workgroup
+constexpr int DQ_VMCNT_ONE_TILE = 5;                  // copies per tile per wave: 3 (K) + 2 (V)
 
 __device__ __forceinline__ void dq_issue(lds_char* smem, const AttnArgs& a, const TileRanges kr, int t, int koff,
                                          int voff, int wave) {
   int row0, pos0, n;
   tile_at(kr, t, DQ_BK, row0, pos0, n);
-  lds_char* dst = smem + (t & 1) * DQ_STAGE;
-  dma_tile<DQK, DQ_BK>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
-  dma_tile<DV, DQ_BK>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
+  lds_char* dst = smem + (t % DQ_NSTAGE) * DQ_STAGE;
+  dma_tile<DQK, DQ_BK, DQ_WAVES>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
+  dma_tile<DV, DQ_BK, DQ_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
 }
 
-__global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * DQ_STAGE];
+__global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem_raw[DQ_NSTAGE * DQ_STAGE];
   lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -74,17 +77,21 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
   if (n_tiles == 0) return;  // uniform over the workgroup
   const int q_row0 = it.row0, q_pos0 = it.pos0, q_n = it.n;
 
-  lds_clear<256>(smem, 2 * DQ_STAGE, tid);
+  lds_clear<64 * DQ_WAVES>(smem, DQ_NSTAGE * DQ_STAGE, tid);
   const int qi = wave * 32 + m;
   const bool q_valid = qi < q_n;
   const int pos_q = q_valid ? q_pos0 + qi : -1;
-  const int lo_q = q_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_q)] : 0;
+  int lo_q = q_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_q)] : 0;
+  // finish this load here: left pending, the tile loop would wait for all copies in flight
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(lo_q)::"memory");
   const int lo_last = a.cu[doc_of(a.cu, a.n_docs, q_pos0 + q_n - 1)];
   const float sl2 = a.scale * LOG2E;
   const int64_t qrow = q_row0 + (q_valid ? qi : 0);
   // invalid rows: LSE = +inf makes P = 0, D = 0 keeps dS = 0
-  const float lse2 = q_valid ? a.lse2[(int64_t)head * a.nq + qrow] : INFINITY;
-  const float Dq = q_valid ? a.Dvec[(int64_t)head * a.nq + qrow] : 0.f;
+  float lse2 = q_valid ? a.lse2[(int64_t)head * a.nq + qrow] : INFINITY;
+  float Dq = q_valid ? a.Dvec[(int64_t)head * a.nq + qrow] : 0.f;
+  settle(lse2);
+  settle(Dq);
   const int koff = dma_lane_off<DQK>(a.H, head, wave, lane);
   const int voff = dma_lane_off<DV>(a.H, head, wave, lane);
 
@@ -96,31 +103,36 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
     for (int t = 0; t < DQK / 16; ++t) {
       u32x4 u = {0u, 0u, 0u, 0u};
       if (q_valid) u = ldg16(qp + 16 * t);
+      settle(u);
       qf[t] = __builtin_bit_cast(bf16x8, u);
     }
 #pragma unroll
     for (int t = 0; t < DV / 16; ++t) {
       u32x4 u = {0u, 0u, 0u, 0u};
       if (q_valid) u = ldg16(dp + 16 * t);
+      settle(u);
       df[t] = __builtin_bit_cast(bf16x8, u);
     }
   }
   __syncthreads();  // LDS cleared before the first copy lands
-  dq_issue(smem, a, kr, 0, koff, voff, wave);
+  for (int t = 0; t < DQ_NSTAGE - 1 && t < n_tiles; ++t) dq_issue(smem, a, kr, t, koff, voff, wave);
 
   f32x16 acc[DQK / 32];
 #pragma unroll
   for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  const OperandOffsets o = operand_offsets(lane);
+  const OperandOffsets o0 = operand_offsets(lane);
 
   for (int t = 0; t < n_tiles; ++t) {
+    const OperandOffsets o = fresh(o0);
     int k_row0, kpos, kn;
     tile_at(kr, t, DQ_BK, k_row0, kpos, kn);
-    wait_dma();
+    // copies of tile t are done once at most one later tile's copies are still in flight
+    if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(DQ_VMCNT_ONE_TILE) : "memory");
+    else wait_dma();
     barrier_lds();
-    if (t + 1 < n_tiles) dq_issue(smem, a, kr, t + 1, koff, voff, wave);
-    const lds_char* Ks = smem + (t & 1) * DQ_STAGE;
+    if (t + DQ_NSTAGE - 1 < n_tiles) dq_issue(smem, a, kr, t + DQ_NSTAGE - 1, koff, voff, wave);
+    const lds_char* Ks = smem + (t % DQ_NSTAGE) * DQ_STAGE;
     const lds_char* Vs = Ks + DQ_KBYTES;
     const bool full = (kn == DQ_BK) && (lo_last <= kpos) && (kpos + DQ_BK - 1 <= q_pos0);
 
@@ -161,6 +173,7 @@ __global__ __launch_bounds__(256, 2) void bwd_dq_kernel(AttnArgs a) {
         for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], dsf[half], acc[c0 + j]);
         if constexpr (gq + 1 < 4)
           op_tr_x3<DQ_BK, 32 * kb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Ks, o, f[(gq + 1) & 1]);
+        sched_fence();
       });
     });
   }
@@ -273,10 +286,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  const OperandOffsets o = operand_offsets(lane);
+  const OperandOffsets o0 = operand_offsets(lane);
   const int poff = pair * 4096 + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
 
   for (int t = 0; t < n_tiles; ++t) {
+    const OperandOffsets o = fresh(o0);
     int q_row0, qpos, qn;
     tile_at(qr, t, KV_BQ, q_row0, qpos, qn);
     // copies of tile t are done once at most one later tile's copies are still in flight
@@ -350,6 +364,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
         for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(f[gq & 1][d], pfr, acc[d]);
         if constexpr (gq + 1 < KV_BQ / 16) op_tr_x4<KV_BQ, 16 * (gq + 1), 0>(Os, o, f[(gq + 1) & 1]);
+        sched_fence();
       });
     } else if (active) {
       static_for<KV_BQ / 32>([&](auto sb_) {
@@ -377,6 +392,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
           for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], sf[half], acc[c0 + j]);
           if constexpr (gq + 1 < 4)
             op_tr_x3<KV_BQ, 32 * sb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Qs, o, f[(gq + 1) & 1]);
+          sched_fence();
         });
       });
     }
@@ -429,7 +445,7 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
     AttnArgs b = a;
     b.n_items = n_qitems;
     tok = prof_begin("bwd_dq", stream);
-    hipLaunchKernelGGL(bwd_dq_kernel, dim3(n_qitems * a.H), dim3(256), 0, stream, b);
+    hipLaunchKernelGGL(bwd_dq_kernel, dim3(n_qitems * a.H), dim3(64 * DQ_WAVES), 0, stream, b);
     prof_end(tok, stream);
     e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -1,10 +1,11 @@
 // Forward partial of one ring step: O = softmax(scale * Q K^T, masked) V and its LSE.
 //
-// One workgroup = 4 waves = 128 query rows of one head; each wave owns 32 rows and keeps
+// One workgroup = 8 waves = 256 query rows of one head; each wave owns 32 rows and keeps
 // them in registers as MFMA B operands for the whole key loop.  Key/value tiles of 64 rows
-// stream through two swizzled LDS stages filled by direct global->LDS copies: the copy of
-// tile t+1 is in flight while tile t is computed, one barrier per tile.  Two workgroups
-// share a CU (2 x 80 KB of LDS), so one's softmax overlaps the other's matrix work.
+// stream through three swizzled LDS stages (120 KB) filled by direct global->LDS copies:
+// the copies of tiles t+1 and t+2 are in flight while tile t is computed, one barrier per
+// tile.  Eight waves share every tile, which halves the L2->LDS traffic per FLOP against a
+// 128-row workgroup; two waves per SIMD let one's softmax overlap the other's matrix work.
 // Scores are computed transposed (S^T = K Q^T), so every lane holds one query and the
 // softmax row reductions stay in-lane plus one exchange with the lane 32 away.
 //
@@ -22,20 +23,25 @@ namespace hydra {
 constexpr int FWD_BK = 64;
 constexpr int FWD_KBYTES = FWD_BK * DQK * 2;             // 24 KB
 constexpr int FWD_STAGE = FWD_KBYTES + FWD_BK * DV * 2;  // 40 KB
+constexpr int FWD_NSTAGE = 3;
+constexpr int FWD_WAVES = 8;
+// Copy instructions one fwd_issue adds per wave: 3 (K) + 2 (V).  Waiting for vmcnt <= 5
+// completes tile t while tile t+1 may stay in flight.
+constexpr int FWD_VMCNT_ONE_TILE = 5;
 constexpr float RESCALE_SLACK = 8.0f;
 
-// Starts the copy of key/value tile t into LDS stage t % 2.
+// Starts the copy of key/value tile t into LDS stage t % FWD_NSTAGE.
 __device__ __forceinline__ void fwd_issue(lds_char* smem, const AttnArgs& a, const TileRanges kr, int t, int koff,
                                           int voff, int head, int wave) {
   int row0, pos0, n;
   tile_at(kr, t, FWD_BK, row0, pos0, n);
-  lds_char* dst = smem + (t & 1) * FWD_STAGE;
-  dma_tile<DQK, FWD_BK>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
-  dma_tile<DV, FWD_BK>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
+  lds_char* dst = smem + (t % FWD_NSTAGE) * FWD_STAGE;
+  dma_tile<DQK, FWD_BK, FWD_WAVES>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
+  dma_tile<DV, FWD_BK, FWD_WAVES>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
 }
 
-__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* __restrict__ o_bf16) {
-  __shared__ __attribute__((aligned(1024))) char smem_raw[2 * FWD_STAGE];
+__global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a, uint16_t* __restrict__ o_bf16) {
+  __shared__ __attribute__((aligned(1024))) char smem_raw[FWD_NSTAGE * FWD_STAGE];
   lds_char* smem = (lds_char*)smem_raw;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -47,12 +53,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
   const TileRanges kr = tile_ranges(it, FWD_BK);
   const int n_tiles = kr.nt;
 
-  lds_clear<256>(smem, 2 * FWD_STAGE, tid);
+  lds_clear<64 * FWD_WAVES>(smem, FWD_NSTAGE * FWD_STAGE, tid);
 
   const int qi = wave * 32 + m;
   const bool q_valid = qi < q_n;
   const int pos_q = q_valid ? q_pos0 + qi : -1;
-  const int lo_q = q_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_q)] : 0;
+  int lo_q = q_valid ? a.cu[doc_of(a.cu, a.n_docs, pos_q)] : 0;
+  // finish this load here: left pending, the tile loop would wait for all copies in flight
+  asm volatile("s_waitcnt vmcnt(0)" : "+v"(lo_q)::"memory");
   const int lo_last = a.cu[doc_of(a.cu, a.n_docs, q_pos0 + q_n - 1)];
   const float sl2 = a.scale * LOG2E;
   const int koff = dma_lane_off<DQK>(a.H, head, wave, lane);
@@ -65,27 +73,31 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
     for (int t = 0; t < DQK / 16; ++t) {
       u32x4 u = {0u, 0u, 0u, 0u};
       if (q_valid) u = ldg16(qrow + 16 * t);
+      settle(u);
       qf[t] = __builtin_bit_cast(bf16x8, u);
     }
   }
   __syncthreads();  // LDS cleared before the first copy lands
 
-  if (n_tiles > 0) fwd_issue(smem, a, kr, 0, koff, voff, head, wave);
+  for (int t = 0; t < FWD_NSTAGE - 1 && t < n_tiles; ++t) fwd_issue(smem, a, kr, t, koff, voff, head, wave);
 
   f32x16 acc[DV / 32];
 #pragma unroll
   for (int d = 0; d < DV / 32; ++d) acc[d] = f32x16{};
-  float m_run = NEG_BIG, l_run = 0.f;
+  float m_run = NEG_BIG, l_run[4] = {0.f, 0.f, 0.f, 0.f};
 
-  const OperandOffsets o = operand_offsets(lane);
+  const OperandOffsets o0 = operand_offsets(lane);
 
   for (int t = 0; t < n_tiles; ++t) {
+    const OperandOffsets o = fresh(o0);
     int k_row0, kpos, kn;
     tile_at(kr, t, FWD_BK, k_row0, kpos, kn);
-    wait_dma();
+    // copies of tile t are done once at most one later tile's copies are still in flight
+    if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(FWD_VMCNT_ONE_TILE) : "memory");
+    else wait_dma();
     barrier_lds();
-    if (t + 1 < n_tiles) fwd_issue(smem, a, kr, t + 1, koff, voff, head, wave);
-    const lds_char* Ks = smem + (t & 1) * FWD_STAGE;
+    if (t + FWD_NSTAGE - 1 < n_tiles) fwd_issue(smem, a, kr, t + FWD_NSTAGE - 1, koff, voff, head, wave);
+    const lds_char* Ks = smem + (t % FWD_NSTAGE) * FWD_STAGE;
     const lds_char* Vs = Ks + FWD_KBYTES;
 
     f32x16 s[2];
@@ -98,46 +110,50 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
     }
 
     const bool full = (kn == FWD_BK) && (lo_last <= kpos) && (kpos + FWD_BK - 1 <= q_pos0);
-    float mx = -INFINITY;
-    if (full) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmax2(mx, s[kb][e]);
-    } else {
+    if (!full) {
+      // key kpos + key(e) is visible iff lo_q <= it <= pos_q and key(e) < kn, i.e. iff
+      // 0 <= base + c(e) < lim with base = kpos - lo_q + 8*hh
+      const int base = kpos - lo_q + 8 * hh;
+      const int lim = q_valid ? max(0, min(pos_q + 1, kpos + kn) - lo_q) : 0;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int key = kb * 32 + 16 * (e >> 3) + 8 * hh + (e & 7);
-          const int kp = kpos + key;
-          const bool vis = (key < kn) && (kp <= pos_q) && (kp >= lo_q);
-          s[kb][e] = vis ? s[kb][e] : -INFINITY;
-          mx = fmax2(mx, s[kb][e]);
+          const int r = base + 32 * kb + 16 * (e >> 3) + (e & 7);
+          s[kb][e] = (unsigned)r < (unsigned)lim ? s[kb][e] : -INFINITY;
         }
     }
+    // row max as a tree of independent chains (short dependency chains)
+    float mx4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x16& v = s[j >> 1];
+      const int e0 = 8 * (j & 1);
+      mx4[j] = fmax2(fmax2(fmax2(v[e0], v[e0 + 1]), fmax2(v[e0 + 2], v[e0 + 3])),
+                     fmax2(fmax2(v[e0 + 4], v[e0 + 5]), fmax2(v[e0 + 6], v[e0 + 7])));
+    }
+    const float mx = fmax2(fmax2(mx4[0], mx4[1]), fmax2(mx4[2], mx4[3]));
     const float mxs = xhalf_max(mx) * sl2;  // -inf when nothing is visible
     if (__builtin_amdgcn_ballot_w64(mxs > m_run + RESCALE_SLACK) != 0) {
       const float m_new = mxs > m_run + RESCALE_SLACK ? mxs : m_run;
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
-      l_run *= alpha;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) l_run[j] *= alpha;
 #pragma unroll
       for (int d = 0; d < DV / 32; ++d) acc[d] *= alpha;
     }
     const float neg_m = -m_run;
 
+    // P = exp2(s*scale*log2e - m); the row sum is kept as four partial sums
     bf16x8 pf[4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      float p[16];
+    for (int j = 0; j < 4; ++j) {
+      float p[8];
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kb][e], sl2, neg_m));
-        l_run += p[e];
-      }
-      pf[2 * kb] = to_bf16x8(p);
-      pf[2 * kb + 1] = to_bf16x8(p + 8);
+      for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j >> 1][8 * (j & 1) + e], sl2, neg_m));
+      l_run[j] += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+      pf[j] = to_bf16x8(p);
     }
 
     // O^T[dv][q] += V^T[dv][key] * P^T[key][q]; V^T fragments via LDS transpose reads.  The
@@ -152,7 +168,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
     });
   }
 
-  const float l_tot = xhalf_sum(l_run);
+  const float l_tot = xhalf_sum((l_run[0] + l_run[1]) + (l_run[2] + l_run[3]));
   if (q_valid) {
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
     const int64_t base = ((int64_t)(q_row0 + qi) * a.H + head) * DV + 4 * hh;
@@ -178,7 +194,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(AttnArgs a, uint16_t* 
 hipError_t launch_attn_fwd(const AttnArgs& a, uint16_t* o_bf16, hipStream_t stream) {
   if (a.n_items == 0) return hipSuccess;
   const int tok = prof_begin("attn_fwd", stream);
-  hipLaunchKernelGGL(attn_fwd_kernel, dim3(a.n_items * a.H), dim3(256), 0, stream, a, o_bf16);
+  hipLaunchKernelGGL(attn_fwd_kernel, dim3(a.n_items * a.H), dim3(64 * FWD_WAVES), 0, stream, a, o_bf16);
   prof_end(tok, stream);
   return hipGetLastError();
 }

@@ -141,6 +141,20 @@ __device__ __forceinline__ OperandOffsets operand_offsets(int lane) {
   return o;
 }
 
+// Re-issues the offsets as opaque values at the top of each tile iteration: otherwise the
+// compiler hoists every (offset + immediate) sum out of the tile loop, one register each,
+// instead of folding the immediate into the read's offset field.
+__device__ __forceinline__ OperandOffsets fresh(const OperandOffsets& o) {
+  OperandOffsets r = o;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(r.b128[j]));
+#pragma unroll
+  for (int v = 0; v < 2; ++v)
+#pragma unroll
+    for (int k = 0; k < 2; ++k) asm volatile("" : "+v"(r.tr[v][k]));
+  return r;
+}
+
 __device__ __forceinline__ bf16x8 lds_ld16(const lds_char* base, int off) {
   return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(base + off);
 }
@@ -151,15 +165,11 @@ __device__ __forceinline__ bf16x8 op_b128(const lds_char* tile, const OperandOff
   return lds_ld16(tile, o.b128[t & 3] + (t >> 2) * block_bytes<ROWS>() + row_block * 128);
 }
 
-// ------------------------------------------------------------------ LDS reads as inline assembly
-// The compiler's wait insertion treats the transpose-read builtin, and any LDS access after a
-// direct-to-LDS copy, as a possible alias of every copy still in flight (including the
-// prefetch into another stage) and waits for all of them first.  The reads below are
-// therefore inline assembly.  Each group of reads and its s_waitcnt are ONE asm statement
-// with early-clobber outputs: a read's destination registers are written when the data
-// arrives, so no instruction may touch them (not even a register copy the allocator might
-// insert) until the wait.  Offsets that are compile-time constants travel in the
-// instruction's offset field.
+// ------------------------------------------------------------------ LDS operand reads
+// Plain LDS loads and the transpose-read builtin: the compiler schedules them ahead of their
+// uses and waits for exactly the reads it needs.  It never sees the direct-to-LDS copies
+// (those are inline assembly, below), so it never waits for a copy still in flight; the
+// kernels wait for their copies explicitly and publish them with a barrier.
 
 template <int N> struct IntC { static constexpr int value = N; };
 
@@ -180,103 +190,66 @@ __device__ __forceinline__ bf16x8 join(i16x4 lo, i16x4 hi) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-// Transposed operand fragments for column blocks CB0 .. CB0+N-1 (N = 3 or 4) of rows
-// ROWB .. ROWB+15 of a ROWS-row tile (lane pattern of OperandOffsets::tr), read and waited for.
-template <int ROWS, int ROWB, int CB0, int N> struct TrGroup {
-  static constexpr int imm(int n) { return ((CB0 + n) >> 1) * block_bytes<ROWS>() + ROWB * 128; }
-  static constexpr int par(int n) { return (CB0 + n) & 1; }
-};
+__device__ __forceinline__ i16x4 lds_tr8(const lds_char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)(p));
+}
 
+// Transposed operand fragments for column blocks CB0 .. CB0+N-1 of rows ROWB .. ROWB+15 of
+// a ROWS-row tile (lane pattern of OperandOffsets::tr).
+template <int ROWS, int ROWB, int CB0, int N>
+__device__ __forceinline__ void op_tr(const lds_char* tile, const OperandOffsets& o, bf16x8 (&f)[N]) {
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    const lds_char* b = tile + ((CB0 + n) >> 1) * block_bytes<ROWS>() + ROWB * 128;
+    f[n] = join(lds_tr8(b + o.tr[0][(CB0 + n) & 1]), lds_tr8(b + o.tr[1][(CB0 + n) & 1]));
+  }
+}
 template <int ROWS, int ROWB, int CB0>
 __device__ __forceinline__ void op_tr_x4(const lds_char* tile, const OperandOffsets& o, bf16x8 (&f)[4]) {
-  using G = TrGroup<ROWS, ROWB, CB0, 4>;
-  const uint32_t b = lds_addr(tile);
-  i16x4 r0, r1, r2, r3, r4, r5, r6, r7;
-  asm volatile(
-      "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
-      "ds_read_b64_tr_b16 %1, %9 offset:%17\n\t"
-      "ds_read_b64_tr_b16 %2, %10 offset:%18\n\t"
-      "ds_read_b64_tr_b16 %3, %11 offset:%19\n\t"
-      "ds_read_b64_tr_b16 %4, %12 offset:%20\n\t"
-      "ds_read_b64_tr_b16 %5, %13 offset:%21\n\t"
-      "ds_read_b64_tr_b16 %6, %14 offset:%22\n\t"
-      "ds_read_b64_tr_b16 %7, %15 offset:%23\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3), "=&v"(r4), "=&v"(r5), "=&v"(r6), "=&v"(r7)
-      : "v"(b + o.tr[0][G::par(0)]), "v"(b + o.tr[1][G::par(0)]), "v"(b + o.tr[0][G::par(1)]),
-        "v"(b + o.tr[1][G::par(1)]), "v"(b + o.tr[0][G::par(2)]), "v"(b + o.tr[1][G::par(2)]),
-        "v"(b + o.tr[0][G::par(3)]), "v"(b + o.tr[1][G::par(3)]), "i"(G::imm(0)), "i"(G::imm(0)),
-        "i"(G::imm(1)), "i"(G::imm(1)), "i"(G::imm(2)), "i"(G::imm(2)), "i"(G::imm(3)), "i"(G::imm(3))
-      : "memory");
-  f[0] = join(r0, r1);
-  f[1] = join(r2, r3);
-  f[2] = join(r4, r5);
-  f[3] = join(r6, r7);
+  op_tr<ROWS, ROWB, CB0, 4>(tile, o, f);
 }
-
 template <int ROWS, int ROWB, int CB0>
 __device__ __forceinline__ void op_tr_x3(const lds_char* tile, const OperandOffsets& o, bf16x8 (&f)[3]) {
-  using G = TrGroup<ROWS, ROWB, CB0, 3>;
-  const uint32_t b = lds_addr(tile);
-  i16x4 r0, r1, r2, r3, r4, r5;
-  asm volatile(
-      "ds_read_b64_tr_b16 %0, %6 offset:%12\n\t"
-      "ds_read_b64_tr_b16 %1, %7 offset:%13\n\t"
-      "ds_read_b64_tr_b16 %2, %8 offset:%14\n\t"
-      "ds_read_b64_tr_b16 %3, %9 offset:%15\n\t"
-      "ds_read_b64_tr_b16 %4, %10 offset:%16\n\t"
-      "ds_read_b64_tr_b16 %5, %11 offset:%17\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(r0), "=&v"(r1), "=&v"(r2), "=&v"(r3), "=&v"(r4), "=&v"(r5)
-      : "v"(b + o.tr[0][G::par(0)]), "v"(b + o.tr[1][G::par(0)]), "v"(b + o.tr[0][G::par(1)]),
-        "v"(b + o.tr[1][G::par(1)]), "v"(b + o.tr[0][G::par(2)]), "v"(b + o.tr[1][G::par(2)]),
-        "i"(G::imm(0)), "i"(G::imm(0)), "i"(G::imm(1)), "i"(G::imm(1)), "i"(G::imm(2)), "i"(G::imm(2))
-      : "memory");
-  f[0] = join(r0, r1);
-  f[1] = join(r2, r3);
-  f[2] = join(r4, r5);
+  op_tr<ROWS, ROWB, CB0, 3>(tile, o, f);
 }
 
-// Four 16-byte LDS reads at base + lane_off + I0..I3, waited for.
+// Four 16-byte LDS reads at base + lane_off + I0..I3.
 template <int I0, int I1, int I2, int I3>
 __device__ __forceinline__ void lds_x4_f32(const lds_char* base, int lane_off, f32x4& a, f32x4& b, f32x4& c,
                                            f32x4& d) {
-  const uint32_t ad = lds_addr(base) + lane_off;
-  asm volatile(
-      "ds_read_b128 %0, %4 offset:%5\n\t"
-      "ds_read_b128 %1, %4 offset:%6\n\t"
-      "ds_read_b128 %2, %4 offset:%7\n\t"
-      "ds_read_b128 %3, %4 offset:%8\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(a), "=&v"(b), "=&v"(c), "=&v"(d)
-      : "v"(ad), "i"(I0), "i"(I1), "i"(I2), "i"(I3)
-      : "memory");
+  typedef const __attribute__((address_space(3))) f32x4* P;
+  const lds_char* p = base + lane_off;
+  a = *reinterpret_cast<P>(p + I0);
+  b = *reinterpret_cast<P>(p + I1);
+  c = *reinterpret_cast<P>(p + I2);
+  d = *reinterpret_cast<P>(p + I3);
 }
 
-// Two 16-byte LDS reads at base + lane_off + I0, I1, waited for.
+// Two 16-byte LDS reads at base + lane_off + I0, I1.
 template <int I0, int I1>
 __device__ __forceinline__ void lds_x2_bf16(const lds_char* base, int lane_off, bf16x8& a, bf16x8& b) {
-  const uint32_t ad = lds_addr(base) + lane_off;
-  asm volatile(
-      "ds_read_b128 %0, %2 offset:%3\n\t"
-      "ds_read_b128 %1, %2 offset:%4\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&v"(a), "=&v"(b)
-      : "v"(ad), "i"(I0), "i"(I1)
-      : "memory");
+  a = lds_ld16(base + lane_off, I0);
+  b = lds_ld16(base + lane_off, I1);
 }
 
-// 16-byte LDS store of an operand fragment (a hand-off buffer the compiler would otherwise
-// order behind the copies in flight).
+// 16-byte LDS store of an operand fragment.
 template <int I0>
 __device__ __forceinline__ void lds_st16(lds_char* base, int lane_off, bf16x8 v) {
-  const uint32_t ad = lds_addr(base) + lane_off;
-  asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(ad), "v"(v), "i"(I0) : "memory");
+  *reinterpret_cast<__attribute__((address_space(3))) bf16x8*>(base + lane_off + I0) = v;
 }
 
-// N (<= 12) 16-byte global loads from p + 16*t elements... issued and completed in one
-// statement, for operands loaded once before a tile loop (left pending, the compiler would
-// wait for every copy in flight before their uses inside the loop).
+// Keeps the instruction scheduler from moving anything across this point (used between
+// the groups of a software-pipelined loop so that reads are not all hoisted to its top,
+// which would need registers for every group at once).
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Makes the compiler treat x as freshly produced here: a value loaded before a tile loop
+// and passed through settle() right after its load is waited for at that point, not at its
+// first use inside the loop (where the wait would also cover every copy in flight).
+template <class T> __device__ __forceinline__ void settle(T& x) { asm volatile("" : "+v"(x)); }
+
+// Four 16-byte global loads from p + 0, 32, 64, 96 bytes, issued and completed in one
+// statement (operands loaded once before a tile loop).
 __device__ __forceinline__ void ldg_x4(const uint16_t* p, u32x4& a, u32x4& b, u32x4& c, u32x4& d) {
   asm volatile(
       "global_load_dwordx4 %0, %4, off\n\t"
@@ -290,15 +263,47 @@ __device__ __forceinline__ void ldg_x4(const uint16_t* p, u32x4& a, u32x4& b, u3
 }
 
 // ------------------------------------------------------------------ direct global -> LDS copies
-// A buffer resource is built per tile with its base at the tile's first row and its record
+// Copies are inline assembly, invisible to the compiler's wait insertion (see above).  A
+// buffer descriptor is built per tile with its base at the tile's first row and its record
 // count ending at the tile's last valid row, so rows past the end are out of range for the
 // hardware bounds check and never touch memory (all of the offset travels in the VGPR
 // operand, which is what the check covers) (the kernels mask those rows and clear LDS
-// once at start, so whatever the copy leaves there is finite).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* g, int64_t row0, int valid, int H,
-                                                            int dim) {
-  const uint16_t* base = g + row0 * H * (int64_t)dim;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, valid * H * dim * 2, 0x00020000);
+// once at start, so whatever the copy leaves there is finite).  Each copy instruction
+// writes 16 (or 4) bytes per lane at LDS address M0 + 16*lane (4*lane).
+__device__ __forceinline__ u32x4 tile_desc(const void* base, int64_t byte_off, int bytes) {
+  const uint64_t b = (uint64_t)(uintptr_t)base + (uint64_t)byte_off;
+  u32x4 d;
+  d[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  d[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) & 0xffffu;  // stride 0
+  d[2] = __builtin_amdgcn_readfirstlane((uint32_t)bytes);                // record count (bytes)
+  d[3] = 0x00020000u;
+  return d;
+}
+__device__ __forceinline__ u32x4 tile_rsrc(const uint16_t* g, int64_t row0, int valid, int H, int dim) {
+  return tile_desc(g, row0 * H * (int64_t)dim * 2, valid * H * dim * 2);
+}
+
+// One 16-byte-per-lane copy at voff + inc (s_nop: M0 and the descriptor are written by the
+// compiler just before; 5 wait states cover both the M0 and the SGPR-write hazards).
+__device__ __forceinline__ void dma16(uint32_t m0v, u32x4 desc, int voff, int inc) {
+  int tmp;
+  asm volatile(
+      "v_add_u32 %0, %1, %2\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 4\n\t"
+      "buffer_load_dwordx4 %0, %4, 0 offen lds"
+      : "=&v"(tmp)
+      : "s"(inc), "v"(voff), "s"(m0v), "s"(desc)
+      : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(uint32_t m0v, u32x4 desc, int voff) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 4\n\t"
+      "buffer_load_dword %0, %2, 0 offen lds"
+      :
+      : "v"(voff), "s"(m0v), "s"(desc)
+      : "memory", "m0");
 }
 
 // Per-lane byte offset (tile-independent) for dma_tile with NW = 4 or 8 waves.  Lane L of
@@ -311,37 +316,23 @@ template <int DIM> __device__ __forceinline__ int dma_lane_off(int H, int head, 
   return (((8 * wave + q) * H + head) * DIM + lc * 8) * 2;
 }
 
-// voff + inc, computed where it is used: the compiler would otherwise hoist one VGPR per
-// copy instruction out of the tile loop and, under register pressure, spill them (the
-// reloads then wait on every copy in flight).
-__device__ __forceinline__ int add_here(int voff, int inc) {
-  int o;
-  asm volatile("v_add_u32 %0, %1, %2" : "=v"(o) : "s"(inc), "v"(voff));
-  return o;
-}
-
+// Copies a ROWS x DIM tile (NW waves, rows 8j .. 8j+7 of each column block per 1 KB
+// instruction, j = wave + NW*i).  `wave` must be wave-uniform.
 template <int DIM, int ROWS, int NW = 4>
-__device__ __forceinline__ void dma_tile(lds_char* lds, __amdgpu_buffer_rsrc_t rs, int voff, int H, int wave) {
-  typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ void dma_tile(lds_char* lds, u32x4 desc, int voff, int H, int wave) {
   constexpr int NINS = ROWS / 8;  // per column block
   static_assert(NINS % NW == 0, "tile must split evenly over the waves");
+  const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr(lds) + wave * 1024);
 #pragma unroll
   for (int b = 0; b < DIM / 64; ++b)
 #pragma unroll
     for (int i = 0; i < NINS / NW; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + b * block_bytes<ROWS>() + (wave + NW * i) * 1024),
-                                               16,
-                                               (b == 0 && i == 0) ? voff
-                                                                  : add_here(voff, 8 * NW * i * H * DIM * 2 + b * 128),
-                                               0, 0, 0);
+      dma16(base + b * block_bytes<ROWS>() + NW * i * 1024, desc, voff, 8 * NW * i * H * DIM * 2 + b * 128);
 }
 
-// 64 consecutive floats (one per lane) into LDS; entries past `valid` are out of range.
+// 64 fp32 values (valid of them in range) -> LDS, one wave.
 __device__ __forceinline__ void dma_vec64(lds_char* lds, const float* g, int valid, int lane) {
-  typedef __attribute__((address_space(3))) void lds_void;
-  __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(g), (short)0, valid * 4, 0x00020000);
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)lds, 4, lane * 4, 0, 0, 0);
+  dma4(__builtin_amdgcn_readfirstlane(lds_addr(lds)), tile_desc(g, 0, valid * 4), lane * 4);
 }
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }

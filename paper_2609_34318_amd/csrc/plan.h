@@ -10,7 +10,7 @@ namespace hydra {
 
 constexpr int kDqk = 192;
 constexpr int kDv = 128;
-constexpr int kQTile = 128;    // query rows per query-stationary workgroup (4 waves x 32)
+constexpr int kQTile = 256;    // query rows per query-stationary workgroup (8 waves x 32)
 constexpr int kKvTile = 128;   // key rows per key-stationary workgroup (4 waves x 32)
 constexpr int kItemInts = 16;  // int32 per work item
 

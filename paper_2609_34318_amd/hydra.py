@@ -84,6 +84,13 @@ def lib() -> ctypes.CDLL:
         L.hydra_profile_start.restype = ctypes.c_int
         L.hydra_profile_stop.argtypes = [ctypes.POINTER(KernelStat), ctypes.c_int32]
         L.hydra_profile_stop.restype = ctypes.c_int
+        i32, i64 = ctypes.c_int32, ctypes.c_int64
+        for name in ("hydra_pack_heads", "hydra_unpack_heads"):
+            getattr(L, name).argtypes = [i64, i32, i32, i32, vp, vp, vp]
+            getattr(L, name).restype = ctypes.c_int
+        for name in ("hydra_zigzag_gather", "hydra_zigzag_scatter"):
+            getattr(L, name).argtypes = [i64, i64, i32, i32, vp, vp, vp]
+            getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -190,6 +197,36 @@ def lse_merge(o_acc, lse_acc, o_part, lse_part, o_bf16=None, stream=None):
     n_rows, n_heads, d_v = o_acc.shape
     _check(lib().hydra_lse_merge(n_rows, n_heads, d_v, _ptr(o_acc), _ptr(lse_acc), _ptr(o_part),
                                  _ptr(lse_part), _ptr(o_bf16), _stream(stream)), "hydra_lse_merge")
+
+
+# ------------------------------------------------------------------ Ulysses x ring layout
+
+def pack_heads(src, dst, cp_u: int, stream=None):
+    """src [T, H, ...] -> dst [cp_u, T, H/cp_u, ...]: the send buffers of the forward exchange."""
+    T, H = src.shape[0], src.shape[1]
+    hb = src[0, 0].numel() * src.element_size()
+    _check(lib().hydra_pack_heads(T, H, hb, cp_u, _ptr(src), _ptr(dst), _stream(stream)), "hydra_pack_heads")
+
+
+def unpack_heads(src, dst, cp_u: int, stream=None):
+    """src [cp_u, T, H/cp_u, ...] -> dst [T, H, ...]: the inverse of pack_heads."""
+    T, H = dst.shape[0], dst.shape[1]
+    hb = dst[0, 0].numel() * dst.element_size()
+    _check(lib().hydra_unpack_heads(T, H, hb, cp_u, _ptr(src), _ptr(dst), _stream(stream)), "hydra_unpack_heads")
+
+
+def zigzag_gather(src, dst, cp_r: int, r: int, stream=None):
+    """Natural-order rows src [S, ...] -> ring rank r's rows dst [S/cp_r, ...]."""
+    S = src.shape[0]
+    rb = src[0].numel() * src.element_size()
+    _check(lib().hydra_zigzag_gather(S, rb, cp_r, r, _ptr(src), _ptr(dst), _stream(stream)), "hydra_zigzag_gather")
+
+
+def zigzag_scatter(src, dst, cp_r: int, r: int, stream=None):
+    """Ring rank r's rows src [S/cp_r, ...] -> their natural positions in dst [S, ...]."""
+    S = dst.shape[0]
+    rb = dst[0].numel() * dst.element_size()
+    _check(lib().hydra_zigzag_scatter(S, rb, cp_r, r, _ptr(src), _ptr(dst), _stream(stream)), "hydra_zigzag_scatter")
 
 
 def profile_start():

@@ -21,12 +21,36 @@ def _lib():
 
 
 def test_library_exports_every_declared_function():
-    text = open(os.path.join(ROOT, "include", "hydra_attn.h")).read()
-    names = set(re.findall(r"\b(hydra_[a-z0-9_]+)\s*\(", text))
-    assert {"hydra_attn_fwd", "hydra_attn_bwd", "hydra_lse_merge", "hydra_workspace_size"} <= names
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        text = open(os.path.join(ROOT, "include", h)).read()
+        names |= set(re.findall(r"\b(hydra_[a-z0-9_]+)\s*\(", text))
+    assert {"hydra_attn_fwd", "hydra_attn_bwd", "hydra_lse_merge", "hydra_workspace_size",
+            "hydra_pack_heads", "hydra_unpack_heads", "hydra_zigzag_gather", "hydra_zigzag_scatter"} <= names
     L = hydra.lib()
     for n in sorted(names):
         assert hasattr(L, n), f"{n} not exported"
+
+
+def test_layout_arguments_checked_on_host():
+    L = hydra.lib()
+    # heads not divisible by the Ulysses degree, sizes not multiples of 16 bytes, NULL
+    assert L.hydra_pack_heads(8, 6, 256, 4, 16, 1 << 20, None) == -1
+    assert L.hydra_pack_heads(8, 8, 24, 4, 16, 1 << 20, None) == -1
+    assert L.hydra_pack_heads(8, 8, 256, 4, None, 1 << 20, None) == -1
+    assert L.hydra_unpack_heads(-1, 8, 256, 4, 16, 1 << 20, None) == -1
+    # misaligned, overlapping
+    assert L.hydra_pack_heads(8, 8, 256, 4, 24, 1 << 20, None) == -3
+    assert L.hydra_pack_heads(8, 8, 256, 4, 16, 16 + 256, None) == -1
+    assert L.hydra_pack_heads(0, 8, 256, 4, 16, 1 << 20, None) == 0
+    # zigzag: rows must split into 2*cp_r chunks, rank in range, no overlap
+    assert L.hydra_zigzag_gather(30, 64, 4, 0, 16, 1 << 20, None) == -1
+    assert L.hydra_zigzag_gather(32, 64, 4, 4, 16, 1 << 20, None) == -1
+    assert L.hydra_zigzag_gather(32, 64, 4, -1, 16, 1 << 20, None) == -1
+    assert L.hydra_zigzag_gather(32, 40, 4, 0, 16, 1 << 20, None) == -1
+    assert L.hydra_zigzag_scatter(32, 64, 4, 1, 16, 16 + 256, None) == -1
+    assert L.hydra_zigzag_scatter(32, 64, 4, 1, 16, 8, None) == -3
+    assert L.hydra_zigzag_gather(0, 64, 4, 1, 16, 1 << 20, None) == 0
 
 
 def test_status_strings():

@@ -17,6 +17,11 @@ What is computed (the paper's setting, restated):
 * Each step yields a partial output and its log-sum-exp; partials combine
   exactly, as in standard ring CP (Sec. 5.2.2, last paragraph).
 * Under MLA every head has its own K and V (Sec. 1), here d_qk=192, d_v=128.
+  With grouped-query attention a rank holds fewer K/V heads than query heads,
+  h_kv <= h (Sec. 3.5, ring traffic "only the h_kv key/value heads").  How query
+  heads share K/V heads is not printed; the reading used here is the usual one:
+  h_kv contiguous groups of h / h_kv query heads, query head i using K/V head
+  i // (h / h_kv).  h_kv = h is the MLA case.
 
 The attention itself is the textbook masked softmax (the paper names
 FlashAttention, Sec. 1 and Sec. 3.5, and computes the same function):
@@ -65,6 +70,13 @@ def doc_of(cu_seqlens: Sequence[int], pos: np.ndarray) -> np.ndarray:
     return np.searchsorted(cu, pos, side="right") - 1
 
 
+def _group(H: int, Hkv: int) -> int:
+    """Query heads per K/V head."""
+    if Hkv < 1 or H % Hkv:
+        raise ValueError("the K/V head count must divide the query head count")
+    return H // Hkv
+
+
 def _f64(x) -> np.ndarray:
     return np.asarray(x, dtype=np.float64)
 
@@ -81,12 +93,14 @@ def attn_fwd(q, k, v, cu_seqlens, q_segs, kv_segs, scale: Optional[float] = None
              heads: Optional[Iterable[int]] = None, q_rows: Optional[np.ndarray] = None):
     """Partial output and LSE of one ring step.
 
-    q [Nq,H,dqk], k [Nk,H,dqk], v [Nk,H,dv].  Returns O [Nq,H,dv] float64 and
+    q [Nq,H,dqk], k [Nk,Hkv,dqk], v [Nk,Hkv,dv] (Hkv divides H; query head h uses
+    K/V head h // (H/Hkv)).  Returns O [Nq,H,dv] float64 and
     LSE [H,Nq] float64 (natural log).  ``heads`` / ``q_rows`` restrict the work
     to a subset (other entries stay O=0, LSE=-inf); the full-size tests use them.
     """
     Q, K, V = np.asarray(q), np.asarray(k), np.asarray(v)   # promoted to fp64 slice by slice
     nq, H, dqk = Q.shape
+    grp = _group(H, K.shape[1])
     tau = default_scale(dqk) if scale is None else float(scale)
     qpos, kpos = row_positions(q_segs), row_positions(kv_segs)
     assert len(qpos) == nq and len(kpos) == K.shape[0]
@@ -98,7 +112,7 @@ def attn_fwd(q, k, v, cu_seqlens, q_segs, kv_segs, scale: Optional[float] = None
             qi = qi[sel[qi]]
             if len(qi) == 0 or len(ki) == 0:
                 continue
-            Kd, Vd = _f64(K[ki, h, :]), _f64(V[ki, h, :])
+            Kd, Vd = _f64(K[ki, h // grp, :]), _f64(V[ki, h // grp, :])
             step = max(1, _SCORE_BLOCK // len(ki))
             for b in range(0, len(qi), step):
                 rows = qi[b:b + step]
@@ -143,7 +157,8 @@ def attn_bwd(q, k, v, o, lse, do, cu_seqlens, q_segs, kv_segs, scale: Optional[f
              heads: Optional[Iterable[int]] = None, q_rows: Optional[np.ndarray] = None):
     """Gradients of one ring step, given the final merged O and LSE of the rows.
 
-    Returns dQ [Nq,H,dqk] (this step's contribution), dK [Nk,H,dqk], dV [Nk,H,dv].
+    Returns dQ [Nq,H,dqk] (this step's contribution), dK [Nk,Hkv,dqk], dV [Nk,Hkv,dv]
+    (with grouped K/V heads, a K/V head's gradient sums over the query heads of its group).
     ``q_rows`` restricts the queries taken into account: dQ is then computed for
     those rows only, and dK/dV hold only their contributions (complete for a key
     when every query that sees it is selected).
@@ -151,6 +166,7 @@ def attn_bwd(q, k, v, o, lse, do, cu_seqlens, q_segs, kv_segs, scale: Optional[f
     Q, K, V, O, dO = (np.asarray(x) for x in (q, k, v, o, do))   # fp64 slice by slice
     L = _f64(lse)
     nq, H, dqk = Q.shape
+    grp = _group(H, K.shape[1])
     tau = default_scale(dqk) if scale is None else float(scale)
     qpos, kpos = row_positions(q_segs), row_positions(kv_segs)
     dQ = np.zeros(Q.shape)
@@ -163,7 +179,8 @@ def attn_bwd(q, k, v, o, lse, do, cu_seqlens, q_segs, kv_segs, scale: Optional[f
             qi = qi[sel[qi]]
             if len(qi) == 0 or len(ki) == 0:
                 continue
-            Kd, Vd = _f64(K[ki, h, :]), _f64(V[ki, h, :])
+            kh = h // grp
+            Kd, Vd = _f64(K[ki, kh, :]), _f64(V[ki, kh, :])
             step = max(1, _SCORE_BLOCK // len(ki))
             for b in range(0, len(qi), step):
                 rows = qi[b:b + step]
@@ -175,11 +192,11 @@ def attn_bwd(q, k, v, o, lse, do, cu_seqlens, q_segs, kv_segs, scale: Optional[f
                 shift = np.where(np.isfinite(lse_r), lse_r, 0.0)
                 p = np.exp(s - shift[:, None])             # 0 on masked entries
                 p[~np.isfinite(lse_r)] = 0.0
-                dV[ki, h, :] += p.T @ dOr
+                dV[ki, kh, :] += p.T @ dOr
                 dp = dOr @ Vd.T
                 ds = p * (dp - D[rows][:, None])
                 dQ[rows, h, :] += tau * (ds @ Kd)
-                dK[ki, h, :] += tau * (ds.T @ Qr)
+                dK[ki, kh, :] += tau * (ds.T @ Qr)
     return dQ, dK, dV
 
 
@@ -203,24 +220,28 @@ def _visible_ranges(cu_seqlens, qpos, kv_segs):
     return out
 
 
-def uniform_fwd(v, cu_seqlens, q_segs, kv_segs, heads=None):
-    """O and LSE when all logits are equal: O_i = mean of visible v, LSE_i = ln n_i."""
+def uniform_fwd(v, cu_seqlens, q_segs, kv_segs, heads=None, n_q_heads=None):
+    """O and LSE when all logits are equal: O_i = mean of visible v, LSE_i = ln n_i.
+    ``n_q_heads`` (default: as many as V has) gives grouped K/V heads: query head h
+    averages V head h // (n_q_heads / Hkv)."""
     V = _f64(v)
     qpos = row_positions(q_segs)
-    nk, H, dv = V.shape
+    nk, Hkv, dv = V.shape
+    H = Hkv if n_q_heads is None else int(n_q_heads)
+    grp = _group(H, Hkv)
     rng = _visible_ranges(cu_seqlens, qpos, kv_segs)
     n = sum(b - a for a, b in rng).astype(np.float64)
     O = np.zeros((len(qpos), H, dv))
     for h in (range(H) if heads is None else heads):
         pre = np.zeros((nk + 1, dv))
-        np.cumsum(V[:, h, :], axis=0, out=pre[1:])
+        np.cumsum(V[:, h // grp, :], axis=0, out=pre[1:])
         acc = np.zeros((len(qpos), dv))
         for a, b in rng:
             acc += pre[b] - pre[a]
         O[:, h, :] = np.where(n[:, None] > 0, acc / np.maximum(n, 1.0)[:, None], 0.0)
     with np.errstate(divide="ignore"):
         L = np.where(n > 0, np.log(np.maximum(n, 1.0)), NEG_INF)
-    return O, np.broadcast_to(L, (V.shape[1], len(qpos))).copy(), n
+    return O, np.broadcast_to(L, (H, len(qpos))).copy(), n
 
 
 def uniform_bwd_k0(q, v, o, do, n_total, cu_seqlens, q_segs, kv_segs, key_rows,

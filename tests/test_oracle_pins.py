@@ -385,3 +385,77 @@ def test_bf16_rounding_is_nearest_even():
     x = np.array([1.0, 1.00390625, 1.01171875, -2.5e-3, 3.0e38], dtype=np.float32)
     t = torch.tensor(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     np.testing.assert_array_equal(inputs.bf16_round_bits(x), t)
+
+
+# ------------------------------------------------------------ grouped K/V heads (GQA)
+
+@pytest.mark.parametrize("H,Hkv", [(4, 1), (4, 2), (6, 3)])
+def test_gqa_fwd_bwd_equal_mha_on_repeated_heads(H, Hkv):
+    """Grouped K/V heads are the same function as one K/V head per query head with every
+    K/V head repeated over its group; the gradient of a shared head is the sum over its
+    group (chain rule through the repeat).  The reference is torch SDPA on the repeated
+    tensors, so the grouping, the head index map and the reduction are checked against an
+    independent formulation."""
+    cu = [0, 9, 20]
+    segs = [(0, 20)]
+    rng = np.random.default_rng(H * 10 + Hkv)
+    q = rng.standard_normal((20, H, D_QK)) * 0.3
+    k = rng.standard_normal((20, Hkv, D_QK)) * 0.3
+    v = rng.standard_normal((20, Hkv, D_V))
+    g = rng.standard_normal((20, H, D_V))
+    grp = H // Hkv
+    kr, vr = np.repeat(k, grp, axis=1), np.repeat(v, grp, axis=1)   # head i -> K/V head i // grp
+    mask = _block_causal_mask(cu, np.arange(20), np.arange(20))
+    o_ref, (dq_r, dk_r, dv_r) = _sdpa(q, kr, vr, mask=mask, grad=g)
+    O, L = oracle.attn_fwd(q, k, v, cu, segs, segs)
+    assert np.abs(O - o_ref).max() < 1e-12
+    dq, dk, dv = oracle.attn_bwd(q, k, v, O, L, g, cu, segs, segs)
+    assert dk.shape == k.shape and dv.shape == v.shape
+    assert np.abs(dq - dq_r).max() < 1e-11
+    assert np.abs(dk - dk_r.reshape(20, Hkv, grp, D_QK).sum(axis=2)).max() < 1e-11
+    assert np.abs(dv - dv_r.reshape(20, Hkv, grp, D_V).sum(axis=2)).max() < 1e-11
+
+
+def test_gqa_bwd_finite_differences_on_a_shared_head():
+    cu = [0, 6, 11]
+    segs = [(0, 11)]
+    rng = np.random.default_rng(5)
+    q = rng.standard_normal((11, 4, D_QK)) * 0.2
+    k = rng.standard_normal((11, 2, D_QK)) * 0.2
+    v = rng.standard_normal((11, 2, D_V))
+    g = rng.standard_normal((11, 4, D_V))
+    O, L = oracle.attn_fwd(q, k, v, cu, segs, segs)
+    _, dk, dv = oracle.attn_bwd(q, k, v, O, L, g, cu, segs, segs)
+
+    def loss(k_, v_):
+        o, _ = oracle.attn_fwd(q, k_, v_, cu, segs, segs)
+        return float((o * g).sum())
+
+    eps = 1e-6
+    for x, grad, is_k in ((k, dk, True), (v, dv, False)):
+        for idx in ((3, 1, 7), (10, 0, 2), (6, 1, 100)):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += eps
+            xm[idx] -= eps
+            fd = (loss(xp, v) - loss(xm, v)) / (2 * eps) if is_k else (loss(k, xp) - loss(k, xm)) / (2 * eps)
+            assert abs(fd - grad[idx]) <= 1e-6 * max(1.0, abs(fd)), (idx, fd, grad[idx])
+
+
+def test_gqa_rejects_non_divisor_head_counts():
+    q = np.zeros((4, 6, D_QK))
+    k = np.zeros((4, 4, D_QK))
+    v = np.zeros((4, 4, D_V))
+    with pytest.raises(ValueError):
+        oracle.attn_fwd(q, k, v, [0, 4], [(0, 4)], [(0, 4)])
+
+
+def test_gqa_uniform_closed_form_matches_general_oracle():
+    cu = [0, 7, 19]
+    segs = [(0, 19)]
+    rng = np.random.default_rng(9)
+    v = rng.standard_normal((19, 2, D_V))
+    q = np.zeros((19, 6, D_QK))
+    k = rng.standard_normal((19, 2, D_QK))
+    O, L = oracle.attn_fwd(q, k, v, cu, segs, segs)
+    Ou, Lu, _ = oracle.uniform_fwd(v, cu, segs, segs, n_q_heads=6)
+    assert np.abs(O - Ou).max() < 1e-12 and np.abs(L - Lu).max() < 1e-12

@@ -97,6 +97,8 @@ def main() -> int:
     ap.add_argument("--workload", default="zigzag256k_share")
     ap.add_argument("--cpu-rows", type=int, default=2048, help="query rows in the oracle timing sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kv-heads", type=int, default=0,
+                    help="K/V heads (grouped-query attention); 0: one per query head (MLA)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this size first (counter calibration)")
     args = ap.parse_args()
@@ -115,7 +117,12 @@ def main() -> int:
     w = inputs.WORKLOADS[args.workload]
     H = w.n_heads
     t_gen = time.perf_counter()
-    q_b, kv_b, do_b = inputs.make_tensors(w)
+    Hkv = args.kv_heads or H
+    if Hkv == H:
+        q_b, kv_b, do_b = inputs.make_tensors(w)
+    else:  # grouped K/V heads: the same query side, Hkv heads of K and V
+        q_b, _, do_b = inputs.make_tensors(w)
+        kv_b = [(inputs.rows("k", list(st), Hkv, D_QK), inputs.rows("v", list(st), Hkv, D_V)) for st in w.kv_steps]
     if do_b is None:
         do_b = inputs.rows("do", list(w.q_segs), H, D_V)
     dev = lambda b: torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).cuda()
@@ -130,11 +137,11 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    sh = ring.make_share(w.cu_seqlens, H, w.q_segs, w.kv_steps)
+    sh = ring.make_share(w.cu_seqlens, H, w.q_segs, w.kv_steps, n_kv_heads=Hkv)
     pairs_step = [hydra.visible_pairs(p) for p in sh.problems]
     dq = torch.empty((sh.nq, H, D_QK), dtype=torch.float32, device="cuda")
-    dkv = [(torch.empty((k.shape[0], H, D_QK), dtype=torch.float32, device="cuda"),
-            torch.empty((k.shape[0], H, D_V), dtype=torch.float32, device="cuda")) for k, _ in kv]
+    dkv = [(torch.empty((k.shape[0], Hkv, D_QK), dtype=torch.float32, device="cuda"),
+            torch.empty((k.shape[0], Hkv, D_V), dtype=torch.float32, device="cuda")) for k, _ in kv]
 
     def step():
         dq.zero_()
@@ -191,7 +198,7 @@ def main() -> int:
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "seq_len": int(w.cu_seqlens[-1]), "rank_tokens": sh.nq,
-                   "n_heads": H, "d_qk": D_QK, "d_v": D_V, "ring_steps": len(w.kv_steps),
+                   "n_heads": H, "n_kv_heads": Hkv, "d_qk": D_QK, "d_v": D_V, "ring_steps": len(w.kv_steps),
                    "q_segments": [list(s) for s in w.q_segs],
                    "visible_pairs_per_head": pairs_step, "counted_tflop_per_step": round(flop_step / 1e12, 3),
                    "parallelism": "one rank of cp_r=2 x cp_u=8"},

@@ -73,6 +73,9 @@ typedef struct {
   int32_t n_docs;                   /* >= 1                                              */
   hydra_chunk_t q;                  /* this rank's query chunk                           */
   hydra_chunk_t kv;                 /* this ring step's key/value chunk                  */
+  int32_t n_kv_heads;               /* K/V heads held (Sec. 3.5: h_kv <= h); 0 means
+                                       n_heads (MLA).  Must divide n_heads: query head i
+                                       uses K/V head i / (n_heads / n_kv_heads)            */
 } hydra_problem_t;
 
 /* Bytes of device workspace the compute calls need for `p` (host only, no GPU needed).

@@ -101,6 +101,8 @@ AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
   a.lse2 = reinterpret_cast<float*>(base + w.lse2_off);
   a.n_docs = int(pr.cu.size()) - 1;
   a.H = pr.H;
+  a.Hkv = pr.Hkv;
+  a.grp = pr.H / pr.Hkv;
   a.nq = int(pr.nq);
   a.nk = int(pr.nk);
   a.scale = pr.scale;

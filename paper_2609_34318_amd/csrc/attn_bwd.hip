@@ -59,8 +59,8 @@ __device__ __forceinline__ void dq_issue(lds_char* smem, const AttnArgs& a, cons
   int row0, pos0, n;
   tile_at(kr, t, DQ_BK, row0, pos0, n);
   lds_char* dst = smem + (t % DQ_NSTAGE) * DQ_STAGE;
-  dma_tile<DQK, DQ_BK, DQ_WAVES>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
-  dma_tile<DV, DQ_BK, DQ_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
+  dma_tile<DQK, DQ_BK, DQ_WAVES>(dst, tile_rsrc(a.k, row0, n, a.Hkv, DQK), koff, a.Hkv, wave);
+  dma_tile<DV, DQ_BK, DQ_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.Hkv, DV), voff, a.Hkv, wave);
 }
 
 __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
@@ -92,8 +92,9 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
   float Dq = q_valid ? a.Dvec[(int64_t)head * a.nq + qrow] : 0.f;
   settle(lse2);
   settle(Dq);
-  const int koff = dma_lane_off<DQK>(a.H, head, wave, lane);
-  const int voff = dma_lane_off<DV>(a.H, head, wave, lane);
+  const int kv_head = head / a.grp;  // grouped K/V heads: contiguous groups of query heads
+  const int koff = dma_lane_off<DQK>(a.Hkv, kv_head, wave, lane);
+  const int voff = dma_lane_off<DV>(a.Hkv, kv_head, wave, lane);
 
   bf16x8 qf[DQK / 16], df[DV / 16];
   {
@@ -215,14 +216,16 @@ constexpr int KV_PBYTES = 4 * 2 * 2048;                          // P: 4 pairs x
 // tile t+1 may stay in flight (waves 0 and 1 also finish one of t+1's copies).
 constexpr int KV_VMCNT_ONE_TILE = 5;
 
+// Flat tile index t covers (query head of the group, query tile): t = member * nt + tile.
 __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, const TileRanges qr, int t, int qoff,
-                                         int ooff, int head, int wave, int lane) {
+                                         int ooff, int head0, int wave, int lane) {
+  const int member = t / qr.nt, qt = t - member * qr.nt;
   int row0, pos0, n;
-  tile_at(qr, t, KV_BQ, row0, pos0, n);
+  tile_at(qr, qt, KV_BQ, row0, pos0, n);
   lds_char* dst = smem + (t % KV_NSTAGE) * KV_STAGE;
-  dma_tile<DQK, KV_BQ, 8>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff, a.H, wave);
-  dma_tile<DV, KV_BQ, 8>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff, a.H, wave);
-  const int64_t li = (int64_t)head * a.nq + row0;
+  dma_tile<DQK, KV_BQ, 8>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff + member * (DQK * 2), a.H, wave);
+  dma_tile<DV, KV_BQ, 8>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff + member * (DV * 2), a.H, wave);
+  const int64_t li = (int64_t)(head0 + member) * a.nq + row0;
   if (wave == 0) dma_vec64(dst + KV_QBYTES + KV_OBYTES, a.lse2 + li, n, lane);
   if (wave == 1) dma_vec64(dst + KV_QBYTES + KV_OBYTES + KV_BQ * 4, a.Dvec + li, n, lane);
 }
@@ -239,10 +242,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV   role 1: dP, dS, dK
   const int m = lane & 31, hh = lane >> 5;
-  const int head = blockIdx.x % a.H;
-  const Item it(a.items, blockIdx.x / a.H);
+  // one K/V head per workgroup; its dK/dV sum over the group's query heads head0 ..
+  const int kv_head = blockIdx.x % a.Hkv;
+  const int head0 = kv_head * a.grp;
+  const Item it(a.items, blockIdx.x / a.Hkv);
   const TileRanges qr = tile_ranges(it, KV_BQ);
-  const int n_tiles = qr.nt;
+  const int n_tiles = qr.nt * a.grp;  // (query head, query tile) pairs
   if (n_tiles == 0) return;  // uniform over the workgroup
   const int k_row0 = it.row0, k_pos0 = it.pos0, k_n = it.n;
 
@@ -260,14 +265,15 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
       __builtin_amdgcn_readfirstlane(kn_w > 0 ? a.cu[doc_of(a.cu, a.n_docs, wk_first) + 1] : 0);
   const float sl2 = a.scale * LOG2E;
   const int64_t krow = k_row0 + (k_valid ? kj : 0);
-  const int qoff = dma_lane_off<DQK>(a.H, head, wave, lane);
-  const int ooff = dma_lane_off<DV>(a.H, head, wave, lane);
+  const int qoff = dma_lane_off<DQK>(a.H, head0, wave, lane);
+  const int ooff = dma_lane_off<DV>(a.H, head0, wave, lane);
 
   // role A keeps K^T fragments (B operand of S), role B keeps V^T fragments (B operand of dP)
   constexpr int NF = DQK / 16;  // 12 (role B uses the first 8)
   bf16x8 bf[NF];
   {
-    const uint16_t* src = role == 0 ? a.k + (krow * a.H + head) * DQK + 8 * hh : a.v + (krow * a.H + head) * DV + 8 * hh;
+    const uint16_t* src =
+        role == 0 ? a.k + (krow * a.Hkv + kv_head) * DQK + 8 * hh : a.v + (krow * a.Hkv + kv_head) * DV + 8 * hh;
     u32x4 u[NF];
 #pragma unroll
     for (int t = 0; t < NF; ++t) u[t] = u32x4{0u, 0u, 0u, 0u};
@@ -280,7 +286,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
     for (int t = 0; t < NF; ++t) bf[t] = __builtin_bit_cast(bf16x8, u[t]);
   }
   __syncthreads();  // LDS cleared before the first copies land
-  for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head, wave_u, lane);
+  for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head0, wave_u, lane);
 
   f32x16 acc[DQK / 32];  // role A: dV^T (first 4), role B: dK^T (6)
 #pragma unroll
@@ -292,12 +298,12 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   for (int t = 0; t < n_tiles; ++t) {
     const OperandOffsets o = fresh(o0);
     int q_row0, qpos, qn;
-    tile_at(qr, t, KV_BQ, q_row0, qpos, qn);
+    tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
     // copies of tile t are done once at most one later tile's copies are still in flight
     if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
     else wait_dma();
     barrier_lds();
-    if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head, wave_u, lane);
+    if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head0, wave_u, lane);
     const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
     const lds_char* Os = Qs + KV_QBYTES;
     const lds_char* vec_s = Qs + KV_QBYTES + KV_OBYTES;  // LSE2[64] then D[64]
@@ -400,7 +406,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
 
   if (k_valid) {
     if (role == 0) {
-      float* dv = a.dv + (krow * a.H + head) * DV + 4 * hh;
+      float* dv = a.dv + (krow * a.Hkv + kv_head) * DV + 4 * hh;
 #pragma unroll
       for (int d = 0; d < DV / 32; ++d)
 #pragma unroll
@@ -414,7 +420,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
           *p = old;
         }
     } else {
-      float* dk = a.dk + (krow * a.H + head) * DQK + 4 * hh;
+      float* dk = a.dk + (krow * a.Hkv + kv_head) * DQK + 4 * hh;
 #pragma unroll
       for (int c = 0; c < DQK / 32; ++c)
 #pragma unroll
@@ -455,7 +461,7 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
     b.items = kitems;
     b.n_items = n_kitems;
     tok = prof_begin("bwd_dkdv", stream);
-    hipLaunchKernelGGL(bwd_dkdv_kernel, dim3(n_kitems * a.H), dim3(512), 0, stream, b);
+    hipLaunchKernelGGL(bwd_dkdv_kernel, dim3(n_kitems * a.Hkv), dim3(512), 0, stream, b);
     prof_end(tok, stream);
     e = hipGetLastError();
   }

@@ -36,8 +36,8 @@ __device__ __forceinline__ void fwd_issue(lds_char* smem, const AttnArgs& a, con
   int row0, pos0, n;
   tile_at(kr, t, FWD_BK, row0, pos0, n);
   lds_char* dst = smem + (t % FWD_NSTAGE) * FWD_STAGE;
-  dma_tile<DQK, FWD_BK, FWD_WAVES>(dst, tile_rsrc(a.k, row0, n, a.H, DQK), koff, a.H, wave);
-  dma_tile<DV, FWD_BK, FWD_WAVES>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.H, DV), voff, a.H, wave);
+  dma_tile<DQK, FWD_BK, FWD_WAVES>(dst, tile_rsrc(a.k, row0, n, a.Hkv, DQK), koff, a.Hkv, wave);
+  dma_tile<DV, FWD_BK, FWD_WAVES>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.Hkv, DV), voff, a.Hkv, wave);
 }
 
 __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a, uint16_t* __restrict__ o_bf16) {
@@ -63,8 +63,9 @@ __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a,
   asm volatile("s_waitcnt vmcnt(0)" : "+v"(lo_q)::"memory");
   const int lo_last = a.cu[doc_of(a.cu, a.n_docs, q_pos0 + q_n - 1)];
   const float sl2 = a.scale * LOG2E;
-  const int koff = dma_lane_off<DQK>(a.H, head, wave, lane);
-  const int voff = dma_lane_off<DV>(a.H, head, wave, lane);
+  const int kv_head = head / a.grp;  // grouped K/V heads: contiguous groups of query heads
+  const int koff = dma_lane_off<DQK>(a.Hkv, kv_head, wave, lane);
+  const int voff = dma_lane_off<DV>(a.Hkv, kv_head, wave, lane);
 
   bf16x8 qf[DQK / 16];
   {

@@ -412,8 +412,8 @@ __device__ __forceinline__ void tile_at(const TileRanges R, int t, int B, int& r
 
 struct AttnArgs {
   const uint16_t* q;   // [nq][H][192]
-  const uint16_t* k;   // [nk][H][192]
-  const uint16_t* v;   // [nk][H][128]
+  const uint16_t* k;   // [nk][Hkv][192]
+  const uint16_t* v;   // [nk][Hkv][128]
   const uint16_t* o;   // bwd: final O bf16 [nq][H][128]
   const uint16_t* dO;  // bwd: [nq][H][128]
   const float* lse;    // bwd: final LSE [H][nq]
@@ -428,7 +428,9 @@ struct AttnArgs {
   const int* cu;       // document boundaries
   int n_docs;
   int n_items;
-  int H;
+  int H;               // query heads
+  int Hkv;             // K/V heads; query head h uses K/V head h / grp
+  int grp;             // H / Hkv
   int nq, nk;
   float scale;         // softmax scale
 };

@@ -111,7 +111,11 @@ int check_problem(const hydra_problem_t* p, Problem* out) {
   if (nq > kMaxRows || nk > kMaxRows) return HYDRA_ERR_INVALID;
   if (nq * p->n_heads * kDqk >= (int64_t(1) << 40) || nk * p->n_heads * kDqk >= (int64_t(1) << 40))
     return HYDRA_ERR_INVALID;
+  const int hkv = p->n_kv_heads == 0 ? p->n_heads : p->n_kv_heads;
+  if (hkv < 0 || hkv > p->n_heads || p->n_heads % hkv != 0) return HYDRA_ERR_INVALID;
+  if (nk * hkv * kDqk >= (int64_t(1) << 40)) return HYDRA_ERR_INVALID;
   out->H = p->n_heads;
+  out->Hkv = hkv;
   out->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt(float(kDqk));
   out->cu.assign(p->cu_seqlens, p->cu_seqlens + p->n_docs + 1);
   out->q = p->q;

@@ -17,6 +17,7 @@ constexpr int kItemInts = 16;  // int32 per work item
 // Checked and normalised view of a hydra_problem_t.
 struct Problem {
   int H = 0;
+  int Hkv = 0;  // K/V heads (divides H)
   float scale = 0.f;
   std::vector<int32_t> cu;     // n_docs + 1 boundaries
   hydra_chunk_t q{}, kv{};

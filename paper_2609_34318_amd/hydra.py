@@ -34,7 +34,8 @@ class ProblemC(ctypes.Structure):
                 ("cu_seqlens", ctypes.POINTER(ctypes.c_int32)),
                 ("n_docs", ctypes.c_int32),
                 ("q", Chunk),
-                ("kv", Chunk)]
+                ("kv", Chunk),
+                ("n_kv_heads", ctypes.c_int32)]
 
 
 class KernelStat(ctypes.Structure):
@@ -111,7 +112,7 @@ class Problem:
     """One ring step of one rank: head shard, documents, Q chunk and KV chunk."""
 
     def __init__(self, cu_seqlens, n_heads: int, q_segs, kv_segs, softmax_scale: float = 0.0,
-                 d_qk: int = 192, d_v: int = 128):
+                 d_qk: int = 192, d_v: int = 128, n_kv_heads: int = 0):
         self.cu = np.ascontiguousarray(np.asarray(cu_seqlens, dtype=np.int32))
         self.q_segs = [tuple(map(int, s)) for s in q_segs]
         self.kv_segs = [tuple(map(int, s)) for s in kv_segs]
@@ -124,7 +125,9 @@ class Problem:
         self.c.n_docs = len(self.cu) - 1
         self.c.q = _chunk(self.q_segs)
         self.c.kv = _chunk(self.kv_segs)
+        self.c.n_kv_heads = n_kv_heads
         self.n_heads = n_heads
+        self.n_kv_heads = n_kv_heads or n_heads
         self.nq = sum(n for _, n in self.q_segs)
         self.nk = sum(n for _, n in self.kv_segs)
 

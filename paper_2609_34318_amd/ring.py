@@ -39,8 +39,9 @@ class Share:
 
 
 def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cuda",
-               softmax_scale: float = 0.0) -> Share:
-    probs = [hydra.Problem(cu_seqlens, n_heads, q_segs, s, softmax_scale) for s in kv_steps]
+               softmax_scale: float = 0.0, n_kv_heads: int = 0) -> Share:
+    """Plans every ring step of one rank; n_kv_heads (0: n_heads) < n_heads for grouped K/V."""
+    probs = [hydra.Problem(cu_seqlens, n_heads, q_segs, s, softmax_scale, n_kv_heads=n_kv_heads) for s in kv_steps]
     ws = max(hydra.workspace_size(p) for p in probs)
     if ws == 0:
         raise hydra.HydraError(-1, "hydra_workspace_size")

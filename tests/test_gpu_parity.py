@@ -31,9 +31,10 @@ def _device():
     torch.cuda.synchronize()
 
 
-def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0):
+def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0, Hkv=0):
     """Forward (and backward if dO given) of a share; returns numpy results."""
-    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale)
+    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale, n_kv_heads=Hkv)
+    Hk = Hkv or H
     q = dev_bf16(q_bits)
     kv = [(dev_bf16(k), dev_bf16(v)) for k, v in kv_bits]
     o, lse, o16 = ring.forward(sh, q, kv)
@@ -41,8 +42,8 @@ def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0):
     if do_bits is not None:
         d_o = dev_bf16(do_bits)
         dq = torch.zeros((sh.nq, H, D_QK), dtype=torch.float32, device="cuda")
-        dkv = [(torch.zeros((k.shape[0], H, D_QK), dtype=torch.float32, device="cuda"),
-                torch.zeros((k.shape[0], H, D_V), dtype=torch.float32, device="cuda")) for k, _ in kv]
+        dkv = [(torch.zeros((k.shape[0], Hk, D_QK), dtype=torch.float32, device="cuda"),
+                torch.zeros((k.shape[0], Hk, D_V), dtype=torch.float32, device="cuda")) for k, _ in kv]
         ring.backward(sh, q, kv, d_o, dq, dkv)
         res["dq"] = dq.cpu().numpy()
         res["dkv"] = [(a.cpu().numpy(), b.cpu().numpy()) for a, b in dkv]
@@ -50,9 +51,10 @@ def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0):
     return res
 
 
-def _gen(cu, H, q_segs, steps, dist="paper", seed=0, bwd=False):
+def _gen(cu, H, q_segs, steps, dist="paper", seed=0, bwd=False, Hkv=0):
+    Hk = Hkv or H
     q = inputs.rows("q", q_segs, H, D_QK, seed, dist)
-    kv = [(inputs.rows("k", s, H, D_QK, seed, dist), inputs.rows("v", s, H, D_V, seed, dist)) for s in steps]
+    kv = [(inputs.rows("k", s, Hk, D_QK, seed, dist), inputs.rows("v", s, Hk, D_V, seed, dist)) for s in steps]
     do = inputs.rows("do", q_segs, H, D_V, seed, dist) if bwd else None
     return q, kv, do
 
@@ -133,6 +135,24 @@ def test_medium_forward_backward(layout, dist):
     ref = _oracle_share(cu, q_segs, steps, q, kv, do)
     _check_fwd(res, ref)
     _check_bwd(res, ref)
+
+
+@pytest.mark.parametrize("layout", ["ragged_3step", "zigzag_2step"])
+@pytest.mark.parametrize("H,Hkv", [(8, 1), (8, 2), (6, 3)])
+def test_gqa_medium_forward_backward(layout, H, Hkv):
+    """Grouped K/V heads: query head i uses K/V head i // (H/Hkv); dK/dV of a K/V head sum
+    over its group (the dK/dV kernel walks the group's query heads one after another)."""
+    cu, q_segs, steps = MEDIUM[layout]
+    q, kv, do = _gen(cu, H, q_segs, steps, dist="sharp", seed=2, bwd=True, Hkv=Hkv)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do, Hkv=Hkv)
+    ref = _oracle_share(cu, q_segs, steps, q, kv, do)
+    _check_fwd(res, ref)
+    _check_bwd(res, ref)
+
+
+def test_gqa_rejected_when_groups_do_not_divide():
+    p = hydra.Problem([0, 64], 6, [(0, 64)], [(0, 64)], n_kv_heads=4)
+    assert hydra.lib().hydra_workspace_size(p.ref) == 0
 
 
 def test_nondefault_scale():
@@ -264,6 +284,28 @@ def test_ring256k_three_steps_uniform_closed_form_and_sampled_rows():
     assert_lse_close(res["lse"][heads][:, rows], L[:, rows])
     res_c = _run_share(cu, H, q_segs, [steps[2]], q, [kv[2]])
     assert np.isneginf(res_c["lse"]).all() and (res_c["o"] == 0).all()
+
+
+def test_gqa_zigzag256k_share_uniform_forward_and_sampled_rows():
+    """The benchmark share with 16 query heads over 2 K/V heads: Q = 0 closed form on every
+    element, then real inputs on sampled rows of two heads of different groups."""
+    w = inputs.WORKLOADS["zigzag256k_share"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    Hkv = 2
+    q, kv, _ = _gen(cu, H, q_segs, steps, Hkv=Hkv)
+    res = _run_share(cu, H, q_segs, steps, np.zeros_like(q), kv, Hkv=Hkv)
+    v_all = np.concatenate([f32(v) for _, v in kv])
+    Uo, UL, _ = oracle.uniform_fwd(v_all, cu, q_segs, _union(steps), n_q_heads=H)
+    assert_lse_close(res["lse"], UL)
+    assert_o_close(res["o"], Uo)
+    res = _run_share(cu, H, q_segs, steps, q, kv, Hkv=Hkv)
+    rows = _sample_rows(131072, [0, 65535, 65536, 131071], 12, 4)
+    heads = [5, 9]                      # groups 0 and 1
+    k_all = np.concatenate([f32(k) for k, _ in kv])
+    O, L = oracle.attn_fwd(f32(q)[:, heads], k_all[:, [0, 1]], v_all[:, [0, 1]], cu, q_segs, _union(steps),
+                           q_rows=rows)
+    assert_o_close(res["o"][rows][:, heads], O[rows])
+    assert_lse_close(res["lse"][heads][:, rows], L[:, rows])
 
 
 def test_packed32k_backward_full_heads():

@@ -38,6 +38,27 @@ class ProblemC(ctypes.Structure):
                 ("n_kv_heads", ctypes.c_int32)]
 
 
+class SchedConfig(ctypes.Structure):
+    _fields_ = [("n_ranks", ctypes.c_int32),
+                ("token_budget", ctypes.c_int64),
+                ("pp", ctypes.c_int32),
+                ("theta_over_c", ctypes.c_double),
+                ("cap", ctypes.c_int32),
+                ("balance_ratio", ctypes.c_double)]
+
+
+class SchedSummary(ctypes.Structure):
+    _fields_ = [("w_hi", ctypes.c_int64),
+                ("w_lo", ctypes.c_int64),
+                ("s_max", ctypes.c_int64),
+                ("c_mem", ctypes.c_int32),
+                ("c_hat", ctypes.c_double),
+                ("cap", ctypes.c_int32),
+                ("m_target", ctypes.c_int64),
+                ("n_mbs", ctypes.c_int32),
+                ("max_load_x_cap", ctypes.c_int64)]
+
+
 class KernelStat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 32),
                 ("launches", ctypes.c_int64),
@@ -89,6 +110,10 @@ def lib() -> ctypes.CDLL:
         for name in ("hydra_pack_heads", "hydra_unpack_heads"):
             getattr(L, name).argtypes = [i64, i32, i32, i32, vp, vp, vp]
             getattr(L, name).restype = ctypes.c_int
+        L.hydra_schedule.argtypes = [ctypes.POINTER(ctypes.c_int64), i64, ctypes.POINTER(SchedConfig),
+                                     ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32),
+                                     ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(SchedSummary)]
+        L.hydra_schedule.restype = ctypes.c_int
         for name in ("hydra_zigzag_gather", "hydra_zigzag_scatter"):
             getattr(L, name).argtypes = [i64, i64, i32, i32, vp, vp, vp]
             getattr(L, name).restype = ctypes.c_int
@@ -230,6 +255,25 @@ def zigzag_scatter(src, dst, cp_r: int, r: int, stream=None):
     S = dst.shape[0]
     rb = dst[0].numel() * dst.element_size()
     _check(lib().hydra_zigzag_scatter(S, rb, cp_r, r, _ptr(src), _ptr(dst), _stream(stream)), "hydra_zigzag_scatter")
+
+
+# ------------------------------------------------------------------ scheduler (host only)
+
+def schedule(lengths, n_ranks: int, token_budget: int, pp: int = 1, theta_over_c: float = 0.0, cap: int = 0,
+             balance_ratio: float = 0.0):
+    """Load-driven DCP placement of a batch: per sequence (micro-batch, group start, group
+    size) as three int32 arrays, plus the targets and counts as a dict."""
+    ln = np.ascontiguousarray(np.asarray(lengths, dtype=np.int64))
+    n = ln.size
+    mb, st, sz = (np.empty(n, np.int32) for _ in range(3))
+    cfg = SchedConfig(n_ranks, token_budget, pp, theta_over_c, cap, balance_ratio)
+    summ = SchedSummary()
+    p32 = lambda a: a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    _check(lib().hydra_schedule(ln.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), n, ctypes.byref(cfg), p32(mb),
+                                p32(st), p32(sz), ctypes.byref(summ)), "hydra_schedule")
+    info = {f: getattr(summ, f) for f, _ in SchedSummary._fields_}
+    info["W"] = (info.pop("w_hi") << 62) + info.pop("w_lo")
+    return mb, st, sz, info
 
 
 def profile_start():

@@ -21,7 +21,9 @@ What is computed (the paper's setting, restated):
   product is taken where the output is back in that layout: after the reverse
   (head -> sequence) exchange, i.e. fused with its unpack.  Its backward is fused
   with the pack that starts the backward exchange.
-* Gradients of a loss with output gradient dY' (chain rule; sigmoid' = s (1 - s)):
+* Gradients of a loss with output gradient dY' (chain rule; sigmoid' = s (1 - s),
+  where 1 - s is evaluated as sigmoid(-G), the same number without the cancellation that
+  rounds it to 0 once s rounds to 1):
 
       dY[t, h, d] = dY'[t, h, d] * s[t, h, e]
       dG[t, h, d] = dY'[t, h, d] * Y[t, h, d] * s (1 - s)          (elementwise)
@@ -63,7 +65,7 @@ def gate_bwd(y, g, dy_gated):
     _gate_shape(y, g)
     s = sigmoid(g)
     dy = dyg * s
-    dg = dyg * y * s * (1.0 - s)
+    dg = dyg * y * s * sigmoid(-g)        # 1 - s = sigmoid(-g)
     if g.shape[2] == 1:
         dg = dg.sum(axis=2, keepdims=True)
     return dy, dg

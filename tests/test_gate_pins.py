@@ -66,6 +66,23 @@ def test_gradients_match_finite_differences(e):
         assert abs((loss(y, gp) - loss(y, gm)) / (2 * h) - dg[gi]) < 1e-8
 
 
+@pytest.mark.parametrize("e", [1, 8])
+def test_gate_gradient_at_saturated_logits(e):
+    # sigmoid'(g) = e^-|g| / (1 + e^-|g|)^2 for either sign: tiny but not zero (fp64 holds
+    # e^-100); the relative accuracy must survive s rounding to 1
+    rng = np.random.default_rng(11)
+    y, _, dyg = _inputs(rng, T=2, H=2, d=8, e=e)
+    for gv in (37.0, 60.0, 100.0, -60.0, -100.0):
+        g = np.full((2, 2, e), gv)
+        _, dg = Gt.gate_bwd(y, g, dyg)
+        t = np.exp(-abs(gv))
+        want = dyg * y * (t / (1 + t) ** 2)
+        if e == 1:
+            want = want.sum(axis=2, keepdims=True)
+        assert np.all(dg != 0)
+        assert np.allclose(dg, want, rtol=1e-13, atol=0)
+
+
 @pytest.mark.parametrize("e", [1, 16])
 def test_gradients_match_torch_autograd(e):
     rng = np.random.default_rng(7)

@@ -141,7 +141,9 @@ void hydra_tile_rows(int32_t* q_tile_rows, int32_t* kv_tile_rows);
  * hydra_profile_start() clears earlier records and starts recording.
  * hydra_profile_stop() waits for the recorded events, stops recording, writes up to `cap`
  * per-kernel summaries to `out` and returns the number of distinct kernels (or a negative
- * status).  Names: "attn_fwd", "bwd_pre", "bwd_dq", "bwd_dkdv", "lse_merge". */
+ * status).  Names: "attn_fwd", "bwd_pre", "bwd_dq", "bwd_dkdv", "lse_merge", and for the
+ * calls of hydra_layout.h and hydra_gate.h "pack_heads", "unpack_heads", "zigzag_gather",
+ * "zigzag_scatter", "unpack_gated", "pack_gated_bwd". */
 typedef struct {
   char    name[32];
   int64_t launches;

@@ -39,8 +39,8 @@ extern "C" {
 #endif
 
 /* dst[j][t][k] = src[t][j*(n_heads/cp_u) + k] for j < cp_u, t < n_tokens, k < n_heads/cp_u,
- * each element head_bytes bytes.  n_heads must be a multiple of cp_u.  n_tokens == 0 is a
- * no-op.  Errors: HYDRA_ERR_INVALID (sizes, NULL, overlap), HYDRA_ERR_ALIGN, HYDRA_ERR_HIP. */
+ * each element head_bytes bytes.  n_heads must be a multiple of cp_u; n_tokens <= 2^31 and
+ * n_heads * head_bytes <= 2^34.  n_tokens == 0 is a no-op.  Errors: HYDRA_ERR_INVALID (sizes, NULL, overlap), HYDRA_ERR_ALIGN, HYDRA_ERR_HIP. */
 int hydra_pack_heads(int64_t n_tokens, int32_t n_heads, int32_t head_bytes, int32_t cp_u,
                      const void* src, void* dst, void* stream);
 

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OBJ = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhydra_attn.so")
-SOURCES = ["plan.cpp", "abi.cpp", "sched.cpp", "attn_fwd.hip", "attn_bwd.hip", "lse_merge.hip", "layout.hip"]
+SOURCES = ["plan.cpp", "abi.cpp", "sched.cpp", "attn_fwd.hip", "attn_bwd.hip", "lse_merge.hip", "layout.hip", "gate.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -108,7 +108,9 @@ int pack_common(bool inv, int64_t n_tokens, int32_t n_heads, int32_t head_bytes,
                 void* dst, void* stream) {
   if (n_tokens < 0 || n_heads <= 0 || head_bytes <= 0 || cp_u <= 0) return HYDRA_ERR_INVALID;
   if (n_heads % cp_u != 0 || head_bytes % 16 != 0) return HYDRA_ERR_INVALID;
-  if (n_tokens > (int64_t(1) << 31)) return HYDRA_ERR_INVALID;
+  // one token with every head, in 16-byte units, must fit 32 bits
+  if (n_tokens > (int64_t(1) << 31) || (uint64_t)n_heads * (uint64_t)head_bytes > (uint64_t(1) << 34))
+    return HYDRA_ERR_INVALID;
   if (!src || !dst) return HYDRA_ERR_INVALID;
   if (!aligned16(src) || !aligned16(dst)) return HYDRA_ERR_ALIGN;
   const uint64_t bytes = (uint64_t)n_tokens * n_heads * head_bytes;

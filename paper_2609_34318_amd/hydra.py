@@ -117,6 +117,10 @@ def lib() -> ctypes.CDLL:
         for name in ("hydra_zigzag_gather", "hydra_zigzag_scatter"):
             getattr(L, name).argtypes = [i64, i64, i32, i32, vp, vp, vp]
             getattr(L, name).restype = ctypes.c_int
+        L.hydra_unpack_heads_gated.argtypes = [i64, i32, i32, i32, i32, vp, vp, vp, vp]
+        L.hydra_unpack_heads_gated.restype = ctypes.c_int
+        L.hydra_pack_heads_gated_bwd.argtypes = [i64, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.hydra_pack_heads_gated_bwd.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -255,6 +259,27 @@ def zigzag_scatter(src, dst, cp_r: int, r: int, stream=None):
     S = dst.shape[0]
     rb = dst[0].numel() * dst.element_size()
     _check(lib().hydra_zigzag_scatter(S, rb, cp_r, r, _ptr(src), _ptr(dst), _stream(stream)), "hydra_zigzag_scatter")
+
+
+# ------------------------------------------------------------------ gated output
+
+def unpack_heads_gated(recv, gate, y, stream=None):
+    """recv [cp_u, T, H/cp_u, d_v] bf16, gate logits [T, H, 1 or d_v] bf16 -> y [T, H, d_v] bf16,
+    y = unpacked output * sigmoid(gate)."""
+    cp_u = recv.shape[0]
+    T, H, d_v = y.shape
+    _check(lib().hydra_unpack_heads_gated(T, H, d_v, gate.shape[-1], cp_u, _ptr(recv), _ptr(gate), _ptr(y),
+                                          _stream(stream)), "hydra_unpack_heads_gated")
+
+
+def pack_heads_gated_bwd(y, gate, d_y, d_send, d_gate, stream=None):
+    """Backward of unpack_heads_gated from the gated output y: d_send [cp_u, T, H/cp_u, d_v] and
+    d_gate [T, H, 1 or d_v], all bf16."""
+    cp_u = d_send.shape[0]
+    T, H, d_v = y.shape
+    _check(lib().hydra_pack_heads_gated_bwd(T, H, d_v, gate.shape[-1], cp_u, _ptr(y), _ptr(gate), _ptr(d_y),
+                                            _ptr(d_send), _ptr(d_gate), _stream(stream)),
+           "hydra_pack_heads_gated_bwd")
 
 
 # ------------------------------------------------------------------ scheduler (host only)

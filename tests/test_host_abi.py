@@ -26,7 +26,8 @@ def test_library_exports_every_declared_function():
         text = open(os.path.join(ROOT, "include", h)).read()
         names |= set(re.findall(r"\b(hydra_[a-z0-9_]+)\s*\(", text))
     assert {"hydra_attn_fwd", "hydra_attn_bwd", "hydra_lse_merge", "hydra_workspace_size",
-            "hydra_pack_heads", "hydra_unpack_heads", "hydra_zigzag_gather", "hydra_zigzag_scatter"} <= names
+            "hydra_pack_heads", "hydra_unpack_heads", "hydra_zigzag_gather", "hydra_zigzag_scatter",
+            "hydra_unpack_heads_gated", "hydra_pack_heads_gated_bwd", "hydra_schedule"} <= names
     L = hydra.lib()
     for n in sorted(names):
         assert hasattr(L, n), f"{n} not exported"
@@ -51,6 +52,29 @@ def test_layout_arguments_checked_on_host():
     assert L.hydra_zigzag_scatter(32, 64, 4, 1, 16, 16 + 256, None) == -1
     assert L.hydra_zigzag_scatter(32, 64, 4, 1, 16, 8, None) == -3
     assert L.hydra_zigzag_gather(0, 64, 4, 1, 16, 1 << 20, None) == 0
+
+
+def test_gate_arguments_checked_on_host():
+    L = hydra.lib()
+    a, b, c, d, e = 16, 1 << 24, 2 << 24, 3 << 24, 4 << 24     # disjoint, aligned, never dereferenced
+    f = L.hydra_unpack_heads_gated
+    assert f(8, 8, 128, 1, 3, a, b, c, None) == -1          # heads not a multiple of cp_u
+    assert f(8, 8, 96, 1, 4, a, b, c, None) == -1           # d_v not a power of two
+    assert f(8, 8, 1024, 1, 4, a, b, c, None) == -1         # d_v above 512
+    assert f(8, 8, 128, 8, 4, a, b, c, None) == -1          # gate_dim neither 1 nor d_v
+    assert f(8, 70000, 128, 1, 1, a, b, c, None) == -1      # too many heads
+    assert f(-1, 8, 128, 1, 4, a, b, c, None) == -1
+    assert f(8, 8, 128, 1, 4, None, b, c, None) == -1
+    assert f(8, 8, 128, 1, 4, a + 8, b, c, None) == -3      # misaligned
+    assert f(8, 8, 128, 128, 4, a, b, b + 16, None) == -1   # output overlaps the gate
+    assert f(8, 8, 128, 1, 4, a, b, a + 8 * 8 * 128 * 2 - 16, None) == -1   # ... the input
+    assert f(0, 8, 128, 1, 4, None, None, None, None) == 0  # no rows: no-op
+    g = L.hydra_pack_heads_gated_bwd
+    assert g(8, 8, 128, 1, 4, a, b, c, d, None, None) == -1     # d_gate missing
+    assert g(8, 8, 128, 1, 4, a, b, c, d, e + 4, None) == -3
+    assert g(8, 8, 128, 128, 4, a, b, c, d, d + 16, None) == -1  # the two outputs overlap
+    assert g(8, 8, 128, 1, 4, a, b, c, d, c, None) == -1         # d_gate aliases d_y
+    assert g(0, 8, 128, 1, 4, None, None, None, None, None, None) == 0
 
 
 def test_status_strings():

@@ -122,10 +122,10 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  const OperandOffsets o0 = operand_offsets(lane);
+  OperandOffsets o = operand_offsets(lane);
 
   for (int t = 0; t < n_tiles; ++t) {
-    const OperandOffsets o = fresh(o0);
+    refresh(o);
     int k_row0, kpos, kn;
     tile_at(kr, t, DQ_BK, k_row0, kpos, kn);
     // copies of tile t are done once at most one later tile's copies are still in flight
@@ -292,11 +292,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
 
-  const OperandOffsets o0 = operand_offsets(lane);
+  OperandOffsets o = operand_offsets(lane);
   const int poff = pair * 4096 + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
 
   for (int t = 0; t < n_tiles; ++t) {
-    const OperandOffsets o = fresh(o0);
+    refresh(o);
     int q_row0, qpos, qn;
     tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
     // copies of tile t are done once at most one later tile's copies are still in flight

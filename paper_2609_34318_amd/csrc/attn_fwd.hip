@@ -87,10 +87,10 @@ __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a,
   for (int d = 0; d < DV / 32; ++d) acc[d] = f32x16{};
   float m_run = NEG_BIG, l_run[4] = {0.f, 0.f, 0.f, 0.f};
 
-  const OperandOffsets o0 = operand_offsets(lane);
+  OperandOffsets o = operand_offsets(lane);
 
   for (int t = 0; t < n_tiles; ++t) {
-    const OperandOffsets o = fresh(o0);
+    refresh(o);
     int k_row0, kpos, kn;
     tile_at(kr, t, FWD_BK, k_row0, kpos, kn);
     // copies of tile t are done once at most one later tile's copies are still in flight

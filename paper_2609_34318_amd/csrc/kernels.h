@@ -141,18 +141,17 @@ __device__ __forceinline__ OperandOffsets operand_offsets(int lane) {
   return o;
 }
 
-// Re-issues the offsets as opaque values at the top of each tile iteration: otherwise the
+// Makes the offsets opaque at the top of each tile iteration, in place: otherwise the
 // compiler hoists every (offset + immediate) sum out of the tile loop, one register each,
-// instead of folding the immediate into the read's offset field.
-__device__ __forceinline__ OperandOffsets fresh(const OperandOffsets& o) {
-  OperandOffsets r = o;
+// instead of folding the immediate into the read's offset field.  In place, so that no
+// second copy of the offsets stays live across the loop.
+__device__ __forceinline__ void refresh(OperandOffsets& o) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(r.b128[j]));
+  for (int j = 0; j < 4; ++j) asm volatile("" : "+v"(o.b128[j]));
 #pragma unroll
   for (int v = 0; v < 2; ++v)
 #pragma unroll
-    for (int k = 0; k < 2; ++k) asm volatile("" : "+v"(r.tr[v][k]));
-  return r;
+    for (int k = 0; k < 2; ++k) asm volatile("" : "+v"(o.tr[v][k]));
 }
 
 __device__ __forceinline__ bf16x8 lds_ld16(const lds_char* base, int off) {

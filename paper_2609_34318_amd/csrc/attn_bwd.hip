@@ -235,11 +235,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   lds_char* smem = (lds_char*)smem_raw;
   lds_char* pbuf = smem + KV_NSTAGE * KV_STAGE;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  // The same value, known to the compiler to be wave-uniform: the copy issue selects its
-  // sources with it (a per-lane select there turns each copy into a waterfall loop), while
-  // the role branches keep the per-lane form, under which both roles fit their registers.
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, known to the compiler
   const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV   role 1: dP, dS, dK
   const int m = lane & 31, hh = lane >> 5;
   // one K/V head per workgroup; its dK/dV sum over the group's query heads head0 ..
@@ -267,174 +264,213 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int64_t krow = k_row0 + (k_valid ? kj : 0);
   const int qoff = dma_lane_off<DQK>(a.H, head0, wave, lane);
   const int ooff = dma_lane_off<DV>(a.H, head0, wave, lane);
-
-  // role A keeps K^T fragments (B operand of S), role B keeps V^T fragments (B operand of dP)
-  constexpr int NF = DQK / 16;  // 12 (role B uses the first 8)
-  bf16x8 bf[NF];
-  {
-    const uint16_t* src =
-        role == 0 ? a.k + (krow * a.Hkv + kv_head) * DQK + 8 * hh : a.v + (krow * a.Hkv + kv_head) * DV + 8 * hh;
-    u32x4 u[NF];
-#pragma unroll
-    for (int t = 0; t < NF; ++t) u[t] = u32x4{0u, 0u, 0u, 0u};
-    if (k_valid) {
-      ldg_x4(src, u[0], u[1], u[2], u[3]);
-      ldg_x4(src + 64, u[4], u[5], u[6], u[7]);
-      if (role == 0) ldg_x4(src + 128, u[8], u[9], u[10], u[11]);
-    }
-#pragma unroll
-    for (int t = 0; t < NF; ++t) bf[t] = __builtin_bit_cast(bf16x8, u[t]);
-  }
-  __syncthreads();  // LDS cleared before the first copies land
-  for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head0, wave_u, lane);
-
-  f32x16 acc[DQK / 32];  // role A: dV^T (first 4), role B: dK^T (6)
-#pragma unroll
-  for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
-
-  OperandOffsets o = operand_offsets(lane);
   const int poff = pair * 4096 + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
+  const bool active = kn_w > 0;               // uniform over the pair
 
-  for (int t = 0; t < n_tiles; ++t) {
-    refresh(o);
-    int q_row0, qpos, qn;
-    tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
-    // copies of tile t are done once at most one later tile's copies are still in flight
-    if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
-    else wait_dma();
-    barrier_lds();
-    if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head0, wave_u, lane);
-    const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
-    const lds_char* Os = Qs + KV_QBYTES;
-    const lds_char* vec_s = Qs + KV_QBYTES + KV_OBYTES;  // LSE2[64] then D[64]
-    const bool active = kn_w > 0;                       // uniform over the pair
+  // The two roles run separate copies of the tile loop, with the same copies and the same
+  // two barriers per tile: each copy keeps only its own role's operands and accumulators
+  // live, which leaves registers for reading LDS operands well ahead of their products.
+  auto run = [&](auto role_c) {
+    constexpr int ROLE = decltype(role_c)::value;
+    // role A keeps K^T fragments (B operand of S) and dV^T; role B V^T fragments (B operand
+    // of dP) and dK^T
+    constexpr int NF = ROLE == 0 ? DQK / 16 : DV / 16;
+    constexpr int NACC = ROLE == 0 ? DV / 32 : DQK / 32;
+    bf16x8 bf[NF];
+    {
+      const uint16_t* src = ROLE == 0 ? a.k + (krow * a.Hkv + kv_head) * DQK + 8 * hh
+                                      : a.v + (krow * a.Hkv + kv_head) * DV + 8 * hh;
+      u32x4 u[12];
+#pragma unroll
+      for (int t = 0; t < 12; ++t) u[t] = u32x4{0u, 0u, 0u, 0u};
+      if (k_valid) {
+        ldg_x4(src, u[0], u[1], u[2], u[3]);
+        ldg_x4(src + 64, u[4], u[5], u[6], u[7]);
+        if (ROLE == 0) ldg_x4(src + 128, u[8], u[9], u[10], u[11]);
+      }
+#pragma unroll
+      for (int t = 0; t < NF; ++t) bf[t] = __builtin_bit_cast(bf16x8, u[t]);
+    }
+    __syncthreads();  // LDS cleared before the first copies land
+    for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head0, wave, lane);
 
-    // ---------------- phase 1
-    // What crosses the barrier lives in one set of registers for both roles: role A keeps
-    // P of both sub-blocks (bf16, 16 dwords), role B keeps dP of both sub-blocks.
-    f32x16 carry[2];
-    if (active && role == 0) {
-      static_for<KV_BQ / 32>([&](auto sb_) {
-        constexpr int sb = decltype(sb_)::value;
-        const int qb = qpos + 32 * sb;
-        f32x16 s = f32x16{};
+    f32x16 acc[NACC];
 #pragma unroll
-        for (int t2 = 0; t2 < DQK / 16; ++t2) s = mfma(op_b128<KV_BQ>(Qs, o, 32 * sb, t2), bf[t2], s);
-        // this lane's query rows are 32*sb + 8*hh + {0..7, 16..23}
-        f32x4 l0, l1, l2, l3;
-        lds_x4_f32<128 * sb, 128 * sb + 16, 128 * sb + 64, 128 * sb + 80>(vec_s, 32 * hh, l0, l1, l2, l3);
-        const float lse_r[16] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3],
-                                 l2[0], l2[1], l2[2], l2[3], l3[0], l3[1], l3[2], l3[3]};
-        const bool full = (kn_w == 32) && (qn >= 32 * (sb + 1)) && (wk_last <= qb) && (qb + 31 < hi_first);
-        float p[16];
-        if (full) {
+    for (int c = 0; c < NACC; ++c) acc[c] = f32x16{};
+    OperandOffsets o = operand_offsets(lane);
+
+    for (int t = 0; t < n_tiles; ++t) {
+      refresh(o);
+      int q_row0, qpos, qn;
+      tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
+      // copies of tile t are done once at most one later tile's copies are still in flight
+      if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
+      else wait_dma();
+      barrier_lds();
+      if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head0, wave, lane);
+      const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
+      const lds_char* Os = lds_opaque(Qs + KV_QBYTES);
+      const lds_char* vec_s = lds_opaque(Qs + KV_QBYTES + KV_OBYTES);  // LSE2[64] then D[64]
+
+      if constexpr (ROLE == 0) {
+        // ---------------- phase 1: S, P = exp(S - LSE) (masked), P to LDS for role B
+        bf16x8 pk[4];  // P of this tile, bf16: rows 16*g .. 16*g+15 in pk[g]
+        if (active) {
+          // S of both 32-row sub-blocks.  Left to itself the compiler issues each read just
+          // before its product and waits for it there; instead sub-block 0's reads are all
+          // issued first, and sub-block 1's as sub-block 0's products free their registers.
+          const RowBases qr_b = row_bases(Qs, o);
+          bf16x8 qa[DQK / 16];
 #pragma unroll
-          for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
-        } else {
-          // query row qq = base + c(e) is visible iff lo <= base + c(e) < lim, where base is
-          // this lane's first row relative to its key position; masked entries get exp2(-inf)
-          const int base = qpos - pos_k + 32 * sb + 8 * hh;
-          const int lim = k_valid ? max(0, min(qpos + qn, hi_k) - pos_k) : 0;
+          for (int t2 = 0; t2 < DQK / 16; ++t2) qa[t2] = op_b128<KV_BQ>(qr_b, 0, t2);
+          sched_fence();
+          f32x16 sc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int r = base + 16 * (e >> 3) + (e & 7);
-            const bool vis = (unsigned)r < (unsigned)lim;
-            p[e] = __builtin_amdgcn_exp2f(vis ? __builtin_fmaf(s[e], sl2, -lse_r[e]) : -INFINITY);
+          for (int t2 = 0; t2 < DQK / 16; ++t2) {
+            sc[0] = mfma(qa[t2], bf[t2], sc[0]);
+            qa[t2] = op_b128<KV_BQ>(qr_b, 32, t2);
           }
+          sched_fence();
+#pragma unroll
+          for (int t2 = 0; t2 < DQK / 16; ++t2) sc[1] = mfma(qa[t2], bf[t2], sc[1]);
+          static_for<KV_BQ / 32>([&](auto sb_) {
+            constexpr int sb = decltype(sb_)::value;
+            const int qb = qpos + 32 * sb;
+            const f32x16& s = sc[sb];
+            // this lane's query rows are 32*sb + 8*hh + {0..7, 16..23}
+            f32x4 l0, l1, l2, l3;
+            lds_x4_f32<128 * sb, 128 * sb + 16, 128 * sb + 64, 128 * sb + 80>(vec_s, 32 * hh, l0, l1, l2, l3);
+            const float lse_r[16] = {l0[0], l0[1], l0[2], l0[3], l1[0], l1[1], l1[2], l1[3],
+                                     l2[0], l2[1], l2[2], l2[3], l3[0], l3[1], l3[2], l3[3]};
+            const bool full = (kn_w == 32) && (qn >= 32 * (sb + 1)) && (wk_last <= qb) && (qb + 31 < hi_first);
+            float p[16];
+            if (full) {
+#pragma unroll
+              for (int e = 0; e < 16; ++e) p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], sl2, -lse_r[e]));
+            } else {
+              // query row qq = base + c(e) is visible iff lo <= base + c(e) < lim, where base
+              // is this lane's first row relative to its key position; masked entries get
+              // exp2(-inf)
+              const int base = qpos - pos_k + 32 * sb + 8 * hh;
+              const int lim = k_valid ? max(0, min(qpos + qn, hi_k) - pos_k) : 0;
+#pragma unroll
+              for (int e = 0; e < 16; ++e) {
+                const int r = base + 16 * (e >> 3) + (e & 7);
+                const bool vis = (unsigned)r < (unsigned)lim;
+                p[e] = __builtin_amdgcn_exp2f(vis ? __builtin_fmaf(s[e], sl2, -lse_r[e]) : -INFINITY);
+              }
+            }
+            pk[2 * sb] = to_bf16x8(p);
+            pk[2 * sb + 1] = to_bf16x8(p + 8);
+            lds_st16<2048 * sb>(pbuf, poff, pk[2 * sb]);
+            lds_st16<2048 * sb + 1024>(pbuf, poff, pk[2 * sb + 1]);
+          });
         }
-        const bf16x8 p0 = to_bf16x8(p), p1 = to_bf16x8(p + 8);
-        lds_st16<2048 * sb>(pbuf, poff, p0);
-        lds_st16<2048 * sb + 1024>(pbuf, poff, p1);
-        put_frag(carry[0], 8 * sb, p0);
-        put_frag(carry[0], 8 * sb + 4, p1);
-      });
-    } else if (active) {
+        barrier_lds();  // P of this tile is in LDS
+        // ---------------- phase 2: dV^T[dv][key] += dO^T[dv][q] P[q][key]; groups of four
+        // dO^T fragments, one per 16 query rows; a group's products are issued before the
+        // next group loads
+        if (active) {
+          bf16x8 f[2][4];
+          op_tr_x4<KV_BQ, 0, 0>(Os, o, f[0]);
+          static_for<KV_BQ / 16>([&](auto g_) {
+            constexpr int gq = decltype(g_)::value;
 #pragma unroll
-      for (int sb = 0; sb < KV_BQ / 32; ++sb) {
-        carry[sb] = f32x16{};
+            for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(f[gq & 1][d], pk[gq], acc[d]);
+            if constexpr (gq + 1 < KV_BQ / 16) op_tr_x4<KV_BQ, 16 * (gq + 1), 0>(Os, o, f[(gq + 1) & 1]);
+            sched_fence();
+          });
+        }
+      } else {
+        // ---------------- phase 1: dP = dO V^T of both sub-blocks
+        f32x16 dp[2];
+        if (active) {
+          // reads issued ahead as in role A's S
+          const RowBases or_b = row_bases(Os, o);
+          bf16x8 ob[DV / 16];
 #pragma unroll
-        for (int t2 = 0; t2 < DV / 16; ++t2) carry[sb] = mfma(op_b128<KV_BQ>(Os, o, 32 * sb, t2), bf[t2], carry[sb]);
+          for (int t2 = 0; t2 < DV / 16; ++t2) ob[t2] = op_b128<KV_BQ>(or_b, 0, t2);
+          sched_fence();
+          dp[0] = f32x16{};
+          dp[1] = f32x16{};
+#pragma unroll
+          for (int t2 = 0; t2 < DV / 16; ++t2) {
+            dp[0] = mfma(ob[t2], bf[t2], dp[0]);
+            ob[t2] = op_b128<KV_BQ>(or_b, 32, t2);
+          }
+          sched_fence();
+#pragma unroll
+          for (int t2 = 0; t2 < DV / 16; ++t2) dp[1] = mfma(ob[t2], bf[t2], dp[1]);
+        }
+        barrier_lds();  // P of this tile is in LDS
+        // ---------------- phase 2: dS = P o (dP - D), dK^T[c][key] += Q^T[c][q] dS[q][key]
+        if (active) {
+          static_for<KV_BQ / 32>([&](auto sb_) {
+            constexpr int sb = decltype(sb_)::value;
+            bf16x8 p0, p1;
+            lds_x2_bf16<2048 * sb, 2048 * sb + 1024>(pbuf, poff, p0, p1);
+            f32x4 d0, d1, d2, d3;
+            lds_x4_f32<256 + 128 * sb, 256 + 128 * sb + 16, 256 + 128 * sb + 64, 256 + 128 * sb + 80>(vec_s, 32 * hh,
+                                                                                                      d0, d1, d2, d3);
+            const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
+                                   d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};
+            float ds[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const float pv = (float)(e < 8 ? p0[e] : p1[e - 8]);
+              ds[e] = pv * (dp[sb][e] - D_r[e]);
+            }
+            const bf16x8 sf[2] = {to_bf16x8(ds), to_bf16x8(ds + 8)};
+            // groups of three Q^T column blocks
+            bf16x8 f[2][3];
+            op_tr_x3<KV_BQ, 32 * sb, 0>(Qs, o, f[0]);
+            static_for<4>([&](auto g_) {
+              constexpr int gq = decltype(g_)::value, half = gq >> 1, c0 = 3 * (gq & 1);
+#pragma unroll
+              for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], sf[half], acc[c0 + j]);
+              if constexpr (gq + 1 < 4)
+                op_tr_x3<KV_BQ, 32 * sb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Qs, o, f[(gq + 1) & 1]);
+              sched_fence();
+            });
+          });
+        }
       }
     }
-    barrier_lds();  // P of this tile is in LDS
 
-    // ---------------- phase 2
-    if (active && role == 0) {
-      // dV^T[dv][key] += dO^T[dv][q] P[q][key]; groups of four dO^T fragments, one per
-      // 16 query rows; a group's products are issued before the next group loads.
-      bf16x8 f[2][4];
-      op_tr_x4<KV_BQ, 0, 0>(Os, o, f[0]);
-      static_for<KV_BQ / 16>([&](auto g_) {
-        constexpr int gq = decltype(g_)::value;  // rows 16*gq .. 16*gq+15: sub-block gq/2, half gq%2
-        const bf16x8 pfr = get_frag(carry[0], 4 * gq);
+    if (k_valid) {
+      if constexpr (ROLE == 0) {
+        float* dv = a.dv + (krow * a.Hkv + kv_head) * DV + 4 * hh;
 #pragma unroll
-        for (int d = 0; d < DV / 32; ++d) acc[d] = mfma(f[gq & 1][d], pfr, acc[d]);
-        if constexpr (gq + 1 < KV_BQ / 16) op_tr_x4<KV_BQ, 16 * (gq + 1), 0>(Os, o, f[(gq + 1) & 1]);
-        sched_fence();
-      });
-    } else if (active) {
-      static_for<KV_BQ / 32>([&](auto sb_) {
-        constexpr int sb = decltype(sb_)::value;
-        bf16x8 p0, p1;
-        lds_x2_bf16<2048 * sb, 2048 * sb + 1024>(pbuf, poff, p0, p1);
-        f32x4 d0, d1, d2, d3;
-        lds_x4_f32<256 + 128 * sb, 256 + 128 * sb + 16, 256 + 128 * sb + 64, 256 + 128 * sb + 80>(vec_s, 32 * hh, d0,
-                                                                                                  d1, d2, d3);
-        const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
-                               d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};
-        float ds[16];
+        for (int d = 0; d < DV / 32; ++d)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float pv = (float)(e < 8 ? p0[e] : p1[e - 8]);
-          ds[e] = pv * (carry[sb][e] - D_r[e]);
-        }
-        const bf16x8 sf[2] = {to_bf16x8(ds), to_bf16x8(ds + 8)};
-        // dK^T[c][key] += Q^T[c][q] dS[q][key]; groups of three Q^T column blocks
-        bf16x8 f[2][3];
-        op_tr_x3<KV_BQ, 32 * sb, 0>(Qs, o, f[0]);
-        static_for<4>([&](auto g_) {
-          constexpr int gq = decltype(g_)::value, half = gq >> 1, c0 = 3 * (gq & 1);
+          for (int rr = 0; rr < 4; ++rr) {
+            f32x4* p = reinterpret_cast<f32x4*>(dv + 32 * d + 8 * rr);
+            f32x4 old = *p;
+            old[0] += acc[d][4 * rr];
+            old[1] += acc[d][4 * rr + 1];
+            old[2] += acc[d][4 * rr + 2];
+            old[3] += acc[d][4 * rr + 3];
+            *p = old;
+          }
+      } else {
+        float* dk = a.dk + (krow * a.Hkv + kv_head) * DQK + 4 * hh;
 #pragma unroll
-          for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], sf[half], acc[c0 + j]);
-          if constexpr (gq + 1 < 4)
-            op_tr_x3<KV_BQ, 32 * sb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Qs, o, f[(gq + 1) & 1]);
-          sched_fence();
-        });
-      });
+        for (int c = 0; c < DQK / 32; ++c)
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            f32x4* p = reinterpret_cast<f32x4*>(dk + 32 * c + 8 * rr);
+            f32x4 old = *p;
+            old[0] += a.scale * acc[c][4 * rr];
+            old[1] += a.scale * acc[c][4 * rr + 1];
+            old[2] += a.scale * acc[c][4 * rr + 2];
+            old[3] += a.scale * acc[c][4 * rr + 3];
+            *p = old;
+          }
+      }
     }
-  }
-
-  if (k_valid) {
-    if (role == 0) {
-      float* dv = a.dv + (krow * a.Hkv + kv_head) * DV + 4 * hh;
-#pragma unroll
-      for (int d = 0; d < DV / 32; ++d)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          f32x4* p = reinterpret_cast<f32x4*>(dv + 32 * d + 8 * rr);
-          f32x4 old = *p;
-          old[0] += acc[d][4 * rr];
-          old[1] += acc[d][4 * rr + 1];
-          old[2] += acc[d][4 * rr + 2];
-          old[3] += acc[d][4 * rr + 3];
-          *p = old;
-        }
-    } else {
-      float* dk = a.dk + (krow * a.Hkv + kv_head) * DQK + 4 * hh;
-#pragma unroll
-      for (int c = 0; c < DQK / 32; ++c)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-          f32x4* p = reinterpret_cast<f32x4*>(dk + 32 * c + 8 * rr);
-          f32x4 old = *p;
-          old[0] += a.scale * acc[c][4 * rr];
-          old[1] += a.scale * acc[c][4 * rr + 1];
-          old[2] += a.scale * acc[c][4 * rr + 2];
-          old[3] += a.scale * acc[c][4 * rr + 3];
-          *p = old;
-        }
-    }
-  }
+  };
+  if (role == 0) run(IntC<0>{});
+  else run(IntC<1>{});
 }
 
 hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems,

@@ -158,10 +158,35 @@ __device__ __forceinline__ bf16x8 lds_ld16(const lds_char* base, int off) {
   return *reinterpret_cast<const __attribute__((address_space(3))) bf16x8*>(base + off);
 }
 
+// This lane's four read addresses of b128 operands in a tile (row pi(m), one per 16-byte
+// chunk of a 64-column block), opaque to the compiler: every read is then base + an
+// immediate offset (column block, row block), with no address add per read.  Left to
+// itself the compiler addresses the reads of a phase from its last read, with negative
+// offsets that the unsigned offset field of an LDS read cannot hold.
+struct RowBases {
+  const lds_char* p[4];
+};
+
+__device__ __forceinline__ RowBases row_bases(const lds_char* tile, const OperandOffsets& o) {
+  RowBases r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    r.p[j] = tile + o.b128[j];
+    asm volatile("" : "+v"(r.p[j]));
+  }
+  return r;
+}
+
 // k-step t of a b128 operand at rows row_block + pi(m) of a ROWS-row tile.
 template <int ROWS>
 __device__ __forceinline__ bf16x8 op_b128(const lds_char* tile, const OperandOffsets& o, int row_block, int t) {
   return lds_ld16(tile, o.b128[t & 3] + (t >> 2) * block_bytes<ROWS>() + row_block * 128);
+}
+
+// The same read from opaque bases.
+template <int ROWS>
+__device__ __forceinline__ bf16x8 op_b128(const RowBases& r, int row_block, int t) {
+  return lds_ld16(r.p[t & 3], (t >> 2) * block_bytes<ROWS>() + row_block * 128);
 }
 
 // ------------------------------------------------------------------ LDS operand reads
@@ -182,6 +207,14 @@ template <int N, class F> __device__ __forceinline__ void static_for(F&& f) {
 }
 
 __device__ __forceinline__ uint32_t lds_addr(const lds_char* p) { return (uint32_t)(uintptr_t)p; }
+
+// The same (wave-uniform) LDS address, opaque to the compiler.  Without it the compiler
+// addresses one tile's reads as offsets from another tile's base, and the negative ones do
+// not fit the unsigned offset field of an LDS read, so each costs its own address add.
+__device__ __forceinline__ const lds_char* lds_opaque(const lds_char* p) {
+  asm volatile("" : "+s"(p));
+  return p;
+}
 
 __device__ __forceinline__ bf16x8 join(i16x4 lo, i16x4 hi) {
   typedef short i16x8 __attribute__((ext_vector_type(8)));

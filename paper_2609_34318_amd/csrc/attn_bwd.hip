@@ -211,23 +211,26 @@ constexpr int KV_OBYTES = KV_BQ * DV * 2;                        // 16 KB
 constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_BQ * 4;  // + LSE2 and D
 constexpr int KV_NSTAGE = 3;
 constexpr int KV_PBYTES = 4 * 2 * 2048;                          // P: 4 pairs x 2 sub-blocks x 32x32 bf16
-// Vector-memory instructions one kv_issue adds per wave (8 waves): 3 (Q) + 2 (dO) copies,
-// plus one vector copy on waves 0 and 1.  Waiting for vmcnt <= 5 completes tile t while
-// tile t+1 may stay in flight (waves 0 and 1 also finish one of t+1's copies).
-constexpr int KV_VMCNT_ONE_TILE = 5;
+// The copies are issued by the four role-B waves only (role A's first phase is the longer
+// one).  Vector-memory instructions one kv_issue adds per issuing wave: 6 (Q) + 4 (dO)
+// copies, plus one vector copy on waves b = 0 and 1.  Waiting for vmcnt <= 10 completes
+// tile t while tile t+1 may stay in flight (waves b = 0 and 1 also finish one of t+1's
+// copies).
+constexpr int KV_VMCNT_ONE_TILE = 10;
 
 // Flat tile index t covers (query head of the group, query tile): t = member * nt + tile.
+// wave_b: 0 .. 3, the issuing wave among the role-B waves.
 __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, const TileRanges qr, int t, int qoff,
-                                         int ooff, int head0, int wave, int lane) {
+                                         int ooff, int head0, int wave_b, int lane) {
   const int member = t / qr.nt, qt = t - member * qr.nt;
   int row0, pos0, n;
   tile_at(qr, qt, KV_BQ, row0, pos0, n);
   lds_char* dst = smem + (t % KV_NSTAGE) * KV_STAGE;
-  dma_tile<DQK, KV_BQ, 8>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff + member * (DQK * 2), a.H, wave);
-  dma_tile<DV, KV_BQ, 8>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff + member * (DV * 2), a.H, wave);
+  dma_tile<DQK, KV_BQ, 4>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff + member * (DQK * 2), a.H, wave_b);
+  dma_tile<DV, KV_BQ, 4>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff + member * (DV * 2), a.H, wave_b);
   const int64_t li = (int64_t)(head0 + member) * a.nq + row0;
-  if (wave == 0) dma_vec64(dst + KV_QBYTES + KV_OBYTES, a.lse2 + li, n, lane);
-  if (wave == 1) dma_vec64(dst + KV_QBYTES + KV_OBYTES + KV_BQ * 4, a.Dvec + li, n, lane);
+  if (wave_b == 0) dma_vec64(dst + KV_QBYTES + KV_OBYTES, a.lse2 + li, n, lane);
+  if (wave_b == 1) dma_vec64(dst + KV_QBYTES + KV_OBYTES + KV_BQ * 4, a.Dvec + li, n, lane);
 }
 
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
@@ -262,8 +265,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
       __builtin_amdgcn_readfirstlane(kn_w > 0 ? a.cu[doc_of(a.cu, a.n_docs, wk_first) + 1] : 0);
   const float sl2 = a.scale * LOG2E;
   const int64_t krow = k_row0 + (k_valid ? kj : 0);
-  const int qoff = dma_lane_off<DQK>(a.H, head0, wave, lane);
-  const int ooff = dma_lane_off<DV>(a.H, head0, wave, lane);
+  const int qoff = dma_lane_off<DQK>(a.H, head0, pair, lane);  // role B's copy lanes (wave b = pair)
+  const int ooff = dma_lane_off<DV>(a.H, head0, pair, lane);
   const int poff = pair * 4096 + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
   const bool active = kn_w > 0;               // uniform over the pair
 
@@ -292,7 +295,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
       for (int t = 0; t < NF; ++t) bf[t] = __builtin_bit_cast(bf16x8, u[t]);
     }
     __syncthreads();  // LDS cleared before the first copies land
-    for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head0, wave, lane);
+    if constexpr (ROLE == 1)
+      for (int t = 0; t < KV_NSTAGE - 1 && t < n_tiles; ++t) kv_issue(smem, a, qr, t, qoff, ooff, head0, pair, lane);
 
     f32x16 acc[NACC];
 #pragma unroll
@@ -304,10 +308,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
       int q_row0, qpos, qn;
       tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
       // copies of tile t are done once at most one later tile's copies are still in flight
-      if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
-      else wait_dma();
+      if constexpr (ROLE == 1) {
+        if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
+        else wait_dma();
+      }
       barrier_lds();
-      if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head0, wave, lane);
+      if constexpr (ROLE == 1)
+        if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head0, pair, lane);
       const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
       const lds_char* Os = lds_opaque(Qs + KV_QBYTES);
       const lds_char* vec_s = lds_opaque(Qs + KV_QBYTES + KV_OBYTES);  // LSE2[64] then D[64]

@@ -89,6 +89,16 @@ def cpu_baseline(w, q, kv, do, budget_rows: int):
                       f"both ring steps + backward of each step ({pairs} visible pairs, {dt:.1f} s)"}
 
 
+# What share of a context-parallel group each workload is (its heads are h / cp_u).
+PARALLELISM = {
+    "zigzag256k_share": "one rank of cp_r=2 x cp_u=8",
+    "ring256k_3step": "one rank of an 8-chunk ring (3 of its steps) x cp_u=8",
+    "packed32k_fwd": "one rank of cp_u=8, no ring",
+    "packed32k_fwdbwd": "one rank of cp_u=8, no ring",
+    "tiny_2step": "one rank, 2 ring steps",
+}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,7 +211,7 @@ def main() -> int:
                    "n_heads": H, "n_kv_heads": Hkv, "d_qk": D_QK, "d_v": D_V, "ring_steps": len(w.kv_steps),
                    "q_segments": [list(s) for s in w.q_segs],
                    "visible_pairs_per_head": pairs_step, "counted_tflop_per_step": round(flop_step / 1e12, 3),
-                   "parallelism": "one rank of cp_r=2 x cp_u=8"},
+                   "parallelism": PARALLELISM.get(w.name, "one rank")},
         "pct_of_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "kernels": kernels,
         "roofline": roofline,

@@ -68,21 +68,6 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const float* v) {
   return __builtin_convertvector(x, bf16x8);
 }
 
-// A bf16 fragment stored in / read from four fp32 register slots of an accumulator-shaped
-// value (register reuse across roles; no data conversion).
-__device__ __forceinline__ void put_frag(f32x16& r, int at, bf16x8 v) {
-  const u32x4 u = __builtin_bit_cast(u32x4, v);
-  r[at] = __uint_as_float(u[0]);
-  r[at + 1] = __uint_as_float(u[1]);
-  r[at + 2] = __uint_as_float(u[2]);
-  r[at + 3] = __uint_as_float(u[3]);
-}
-__device__ __forceinline__ bf16x8 get_frag(const f32x16& r, int at) {
-  u32x4 u = {__float_as_uint(r[at]), __float_as_uint(r[at + 1]), __float_as_uint(r[at + 2]),
-             __float_as_uint(r[at + 3])};
-  return __builtin_bit_cast(bf16x8, u);
-}
-
 __device__ __forceinline__ u32x4 ldg16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 
 // Largest d with cu[d] <= pos (cu has n_docs + 1 entries, pos inside the window).
@@ -105,11 +90,6 @@ __device__ __forceinline__ int doc_of(const int* __restrict__ cu, int n_docs, in
 __device__ __forceinline__ int swz(int r) { return (((r >> 1) & 1) << 2) | ((r >> 2) & 3); }
 
 template <int ROWS> constexpr int block_bytes() { return ROWS * 128; }
-
-// Byte offset of logical 16-byte chunk `c` (0 .. DIM/8-1) of row `r`.
-template <int ROWS> __device__ __forceinline__ int tile_off(int r, int c) {
-  return (c >> 3) * block_bytes<ROWS>() + r * 128 + (((c & 7) ^ swz(r)) << 4);
-}
 
 // Lane-constant parts of the operand reads of a 32x32x16 MFMA from such tiles.
 //   b128[j]: 16-byte read of row pi(m), chunk 2j + h within a column block (k-step t uses

@@ -203,19 +203,19 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
 //   wave A: S = Q K^T, P = exp(S - LSE) (masked), dV^T += dO^T P
 //   wave B: dP = dO V^T, dS = P o (dP - D), dK^T += Q^T dS
 // P crosses from A to B through LDS (rounded to bf16, the value the dV product uses).  Per
-// 64-query tile: barrier, copy the tile two ahead, phase 1 (A: S and P, B: dP), barrier,
-// phase 2 (A: dV, B: dS and dK).
+// 64-query tile: barrier, start the copy of the next tile (LDS holds two), phase 1 (A: S
+// and P, B: dP), barrier, phase 2 (A: dV, B: dS and dK).
 constexpr int KV_BQ = 64;                                        // query rows per tile
 constexpr int KV_QBYTES = KV_BQ * DQK * 2;                       // 24 KB
 constexpr int KV_OBYTES = KV_BQ * DV * 2;                        // 16 KB
 constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_BQ * 4;  // + LSE2 and D
-constexpr int KV_NSTAGE = 3;
+constexpr int KV_NSTAGE = 2;  // measured faster than three stages
 constexpr int KV_PBYTES = 4 * 2 * 2048;                          // P: 4 pairs x 2 sub-blocks x 32x32 bf16
 // The copies are issued by the four role-B waves only (role A's first phase is the longer
 // one).  Vector-memory instructions one kv_issue adds per issuing wave: 6 (Q) + 4 (dO)
-// copies, plus one vector copy on waves b = 0 and 1.  Waiting for vmcnt <= 10 completes
-// tile t while tile t+1 may stay in flight (waves b = 0 and 1 also finish one of t+1's
-// copies).
+// copies, plus one vector copy on waves b = 0 and 1.  With three stages, waiting for
+// vmcnt <= 10 completes tile t while tile t+1 may stay in flight (waves b = 0 and 1 also
+// finish one of t+1's copies); with two, tile t's copies are the only ones in flight.
 constexpr int KV_VMCNT_ONE_TILE = 10;
 
 // Flat tile index t covers (query head of the group, query tile): t = member * nt + tile.
@@ -307,9 +307,10 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
       refresh(o);
       int q_row0, qpos, qn;
       tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
-      // copies of tile t are done once at most one later tile's copies are still in flight
+      // copies of tile t are done once at most the later tiles' copies issued so far (with
+      // two stages: none) are still in flight
       if constexpr (ROLE == 1) {
-        if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
+        if (KV_NSTAGE > 2 && t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KV_VMCNT_ONE_TILE) : "memory");
         else wait_dma();
       }
       barrier_lds();

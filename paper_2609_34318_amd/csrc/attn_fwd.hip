@@ -2,8 +2,8 @@
 //
 // One workgroup = 8 waves = 256 query rows of one head; each wave owns 32 rows and keeps
 // them in registers as MFMA B operands for the whole key loop.  Key/value tiles of 64 rows
-// stream through three swizzled LDS stages (120 KB) filled by direct global->LDS copies:
-// the copies of tiles t+1 and t+2 are in flight while tile t is computed, one barrier per
+// stream through two swizzled LDS stages (80 KB) filled by direct global->LDS copies:
+// the copies of tile t+1 are in flight while tile t is computed, one barrier per
 // tile.  Eight waves share every tile, which halves the L2->LDS traffic per FLOP against a
 // 128-row workgroup; two waves per SIMD let one's softmax overlap the other's matrix work.
 // Scores are computed transposed (S^T = K Q^T), so every lane holds one query and the
@@ -23,10 +23,11 @@ namespace hydra {
 constexpr int FWD_BK = 64;
 constexpr int FWD_KBYTES = FWD_BK * DQK * 2;             // 24 KB
 constexpr int FWD_STAGE = FWD_KBYTES + FWD_BK * DV * 2;  // 40 KB
-constexpr int FWD_NSTAGE = 3;
+constexpr int FWD_NSTAGE = 2;  // measured faster than three stages
 constexpr int FWD_WAVES = 8;
-// Copy instructions one fwd_issue adds per wave: 3 (K) + 2 (V).  Waiting for vmcnt <= 5
-// completes tile t while tile t+1 may stay in flight.
+// Copy instructions one fwd_issue adds per wave: 3 (K) + 2 (V).  With three stages,
+// waiting for vmcnt <= 5 completes tile t while tile t+1 may stay in flight; with two,
+// tile t's copies are the only ones in flight.
 constexpr int FWD_VMCNT_ONE_TILE = 5;
 constexpr float RESCALE_SLACK = 8.0f;
 
@@ -93,8 +94,9 @@ __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a,
     refresh(o);
     int k_row0, kpos, kn;
     tile_at(kr, t, FWD_BK, k_row0, kpos, kn);
-    // copies of tile t are done once at most one later tile's copies are still in flight
-    if (t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(FWD_VMCNT_ONE_TILE) : "memory");
+    // copies of tile t are done once at most the later tiles' copies issued so far (with
+    // two stages: none) are still in flight
+    if (FWD_NSTAGE > 2 && t + 1 < n_tiles) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(FWD_VMCNT_ONE_TILE) : "memory");
     else wait_dma();
     barrier_lds();
     if (t + FWD_NSTAGE - 1 < n_tiles) fwd_issue(smem, a, kr, t + FWD_NSTAGE - 1, koff, voff, head, wave);

@@ -204,14 +204,16 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
 //   wave A: S = Q K^T, P = exp(S - LSE) (masked), dV^T += dO^T P
 //   wave B: dP = dO V^T, dS = P o (dP - D), dK^T += Q^T dS
 // P crosses from A to B through LDS (rounded to bf16, the value the dV product uses).  Per
-// 64-query tile: barrier, start the copy of the next tile (LDS holds two), phase 1 (A: S
+// 96-query tile: barrier, start the copy of the next tile (LDS holds two), phase 1 (A: S
 // and P, B: dP), barrier, phase 2 (A: dV, B: dS and dK).
-constexpr int KV_BQ = 64;                                        // query rows per tile
+constexpr int KV_BQ = 96;                                        // query rows per tile
+constexpr int KV_NSB = KV_BQ / 32;                               // 32-row sub-blocks per tile
+constexpr int KV_VEC = 128;                                      // LDS slots per vector (LSE2, D)
 constexpr int KV_QBYTES = KV_BQ * DQK * 2;                       // 24 KB
 constexpr int KV_OBYTES = KV_BQ * DV * 2;                        // 16 KB
-constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_BQ * 4;  // + LSE2 and D
+constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_VEC * 4;  // + LSE2 and D
 constexpr int KV_NSTAGE = 2;  // measured faster than three stages
-constexpr int KV_PBYTES = 4 * 2 * 2048;                          // P: 4 pairs x 2 sub-blocks x 32x32 bf16
+constexpr int KV_PBYTES = 4 * KV_NSB * 2048;                     // P: 4 pairs x sub-blocks x 32x32 bf16
 // The copies are issued by the four role-B waves only (role A's first phase is the longer
 // one).  Vector-memory instructions one kv_issue adds per issuing wave: 6 (Q) + 4 (dO)
 // copies, plus one vector copy on waves b = 0 and 1.  With three stages, waiting for
@@ -230,8 +232,15 @@ __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, cons
   dma_tile<DQK, KV_BQ, 4>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff + member * (DQK * 2), a.H, wave_b);
   dma_tile<DV, KV_BQ, 4>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff + member * (DV * 2), a.H, wave_b);
   const int64_t li = (int64_t)(head0 + member) * a.nq + row0;
-  if (wave_b == 0) dma_vec64(dst + KV_QBYTES + KV_OBYTES, a.lse2 + li, n, lane);
-  if (wave_b == 1) dma_vec64(dst + KV_QBYTES + KV_OBYTES + KV_BQ * 4, a.Dvec + li, n, lane);
+  // LSE2 and D of the tile's rows, 64 per copy; rows past the tile's end read as zero
+  static_assert(KV_BQ <= 2 * 64 && KV_BQ <= KV_VEC, "two 64-row copies per vector");
+  lds_char* vec = dst + KV_QBYTES + KV_OBYTES;
+  if (wave_b == 0) dma_vec64(vec, a.lse2 + li, min(n, 64), lane);
+  if (wave_b == 1) dma_vec64(vec + KV_VEC * 4, a.Dvec + li, min(n, 64), lane);
+  if constexpr (KV_BQ > 64) {
+    if (wave_b == 2) dma_vec64(vec + 256, a.lse2 + li + 64, max(n - 64, 0), lane);
+    if (wave_b == 3) dma_vec64(vec + KV_VEC * 4 + 256, a.Dvec + li + 64, max(n - 64, 0), lane);
+  }
 }
 
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
@@ -268,7 +277,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int64_t krow = k_row0 + (k_valid ? kj : 0);
   const int qoff = dma_lane_off<DQK>(a.H, head0, pair, lane);  // role B's copy lanes (wave b = pair)
   const int ooff = dma_lane_off<DV>(a.H, head0, pair, lane);
-  const int poff = pair * 4096 + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
+  const int poff = pair * (KV_NSB * 2048) + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
   const bool active = kn_w > 0;               // uniform over the pair
 
   // The two roles run separate copies of the tile loop, with the same copies and the same
@@ -319,29 +328,32 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
         if (t + KV_NSTAGE - 1 < n_tiles) kv_issue(smem, a, qr, t + KV_NSTAGE - 1, qoff, ooff, head0, pair, lane);
       const lds_char* Qs = smem + (t % KV_NSTAGE) * KV_STAGE;
       const lds_char* Os = lds_opaque(Qs + KV_QBYTES);
-      const lds_char* vec_s = lds_opaque(Qs + KV_QBYTES + KV_OBYTES);  // LSE2[64] then D[64]
+      const lds_char* vec_s = lds_opaque(Qs + KV_QBYTES + KV_OBYTES);  // LSE2 then D, KV_VEC slots each
 
       if constexpr (ROLE == 0) {
         // ---------------- phase 1: S, P = exp(S - LSE) (masked), P to LDS for role B
-        bf16x8 pk[4];  // P of this tile, bf16: rows 16*g .. 16*g+15 in pk[g]
+        bf16x8 pk[KV_BQ / 16];  // P of this tile, bf16: rows 16*g .. 16*g+15 in pk[g]
         if (active) {
-          // S of both 32-row sub-blocks.  Left to itself the compiler issues each read just
+          // S of the 32-row sub-blocks.  Left to itself the compiler issues each read just
           // before its product and waits for it there; instead sub-block 0's reads are all
-          // issued first, and sub-block 1's as sub-block 0's products free their registers.
+          // issued first, and each next sub-block's as the current one's products free
+          // their registers.
           const RowBases qr_b = row_bases(Qs, o);
           bf16x8 qa[DQK / 16];
 #pragma unroll
           for (int t2 = 0; t2 < DQK / 16; ++t2) qa[t2] = op_b128<KV_BQ>(qr_b, 0, t2);
           sched_fence();
-          f32x16 sc[2] = {f32x16{}, f32x16{}};
+          f32x16 sc[KV_NSB];
+          static_for<KV_NSB>([&](auto sb_) {
+            constexpr int sb = decltype(sb_)::value;
+            sc[sb] = f32x16{};
 #pragma unroll
-          for (int t2 = 0; t2 < DQK / 16; ++t2) {
-            sc[0] = mfma(qa[t2], bf[t2], sc[0]);
-            qa[t2] = op_b128<KV_BQ>(qr_b, 32, t2);
-          }
-          sched_fence();
-#pragma unroll
-          for (int t2 = 0; t2 < DQK / 16; ++t2) sc[1] = mfma(qa[t2], bf[t2], sc[1]);
+            for (int t2 = 0; t2 < DQK / 16; ++t2) {
+              sc[sb] = mfma(qa[t2], bf[t2], sc[sb]);
+              if constexpr (sb + 1 < KV_NSB) qa[t2] = op_b128<KV_BQ>(qr_b, 32 * (sb + 1), t2);
+            }
+            sched_fence();
+          });
           static_for<KV_BQ / 32>([&](auto sb_) {
             constexpr int sb = decltype(sb_)::value;
             const int qb = qpos + 32 * sb;
@@ -392,7 +404,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
         }
       } else {
         // ---------------- phase 1: dP = dO V^T of both sub-blocks
-        f32x16 dp[2];
+        f32x16 dp[KV_NSB];
         if (active) {
           // reads issued ahead as in role A's S
           const RowBases or_b = row_bases(Os, o);
@@ -400,16 +412,16 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
 #pragma unroll
           for (int t2 = 0; t2 < DV / 16; ++t2) ob[t2] = op_b128<KV_BQ>(or_b, 0, t2);
           sched_fence();
-          dp[0] = f32x16{};
-          dp[1] = f32x16{};
+          static_for<KV_NSB>([&](auto sb_) {
+            constexpr int sb = decltype(sb_)::value;
+            dp[sb] = f32x16{};
 #pragma unroll
-          for (int t2 = 0; t2 < DV / 16; ++t2) {
-            dp[0] = mfma(ob[t2], bf[t2], dp[0]);
-            ob[t2] = op_b128<KV_BQ>(or_b, 32, t2);
-          }
-          sched_fence();
-#pragma unroll
-          for (int t2 = 0; t2 < DV / 16; ++t2) dp[1] = mfma(ob[t2], bf[t2], dp[1]);
+            for (int t2 = 0; t2 < DV / 16; ++t2) {
+              dp[sb] = mfma(ob[t2], bf[t2], dp[sb]);
+              if constexpr (sb + 1 < KV_NSB) ob[t2] = op_b128<KV_BQ>(or_b, 32 * (sb + 1), t2);
+            }
+            sched_fence();
+          });
         }
         barrier_lds();  // P of this tile is in LDS
         // ---------------- phase 2: dS = P o (dP - D), dK^T[c][key] += Q^T[c][q] dS[q][key]
@@ -419,7 +431,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
             bf16x8 p0, p1;
             lds_x2_bf16<2048 * sb, 2048 * sb + 1024>(pbuf, poff, p0, p1);
             f32x4 d0, d1, d2, d3;
-            lds_x4_f32<256 + 128 * sb, 256 + 128 * sb + 16, 256 + 128 * sb + 64, 256 + 128 * sb + 80>(vec_s, 32 * hh,
+            lds_x4_f32<KV_VEC * 4 + 128 * sb, KV_VEC * 4 + 128 * sb + 16, KV_VEC * 4 + 128 * sb + 64,
+                       KV_VEC * 4 + 128 * sb + 80>(vec_s, 32 * hh,
                                                                                                       d0, d1, d2, d3);
             const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
                                    d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};

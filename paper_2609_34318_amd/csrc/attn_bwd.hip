@@ -215,11 +215,11 @@ constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_VEC * 4;  // + LSE2 and 
 constexpr int KV_NSTAGE = 2;  // measured faster than three stages
 constexpr int KV_PBYTES = 4 * KV_NSB * 2048;                     // P: 4 pairs x sub-blocks x 32x32 bf16
 // The copies are issued by the four role-B waves only (role A's first phase is the longer
-// one).  Vector-memory instructions one kv_issue adds per issuing wave: 6 (Q) + 4 (dO)
-// copies, plus one vector copy on waves b = 0 and 1.  With three stages, waiting for
-// vmcnt <= 10 completes tile t while tile t+1 may stay in flight (waves b = 0 and 1 also
-// finish one of t+1's copies); with two, tile t's copies are the only ones in flight.
-constexpr int KV_VMCNT_ONE_TILE = 10;
+// one).  Vector-memory instructions one kv_issue adds per issuing wave: (3 + 2) column
+// blocks x KV_BQ/32 copies of 1 KB (Q, dO), plus one vector copy (LSE2 or D) on each wave
+// that has one.  With three stages, waiting for vmcnt <= KV_VMCNT_ONE_TILE completes tile
+// t while tile t+1 may stay in flight; with two, tile t's copies are the only ones in flight.
+constexpr int KV_VMCNT_ONE_TILE = (DQK / 64 + DV / 64) * (KV_BQ / 32);
 
 // Flat tile index t covers (query head of the group, query tile): t = member * nt + tile.
 // wave_b: 0 .. 3, the issuing wave among the role-B waves.

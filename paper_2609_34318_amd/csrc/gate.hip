@@ -22,10 +22,15 @@ typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
 constexpr int kUnroll = 4;
 constexpr int kThreads = 256;
 
+// Streaming 16-byte accesses: every chunk is touched once, so they bypass cache retention
+// (non-temporal).
+__device__ __forceinline__ u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_stream(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
+
 unsigned grid_for(uint64_t total) {
   const uint64_t per_block = (uint64_t)kThreads * kUnroll;
   const uint64_t want = (total + per_block - 1) / per_block;
-  const uint64_t cap = 256ull * 64;
+  const uint64_t cap = 256ull * 256;
   return (unsigned)(want < cap ? want : cap);
 }
 
@@ -77,10 +82,10 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(const u32x4* __restrict_
       const uint32_t t = (uint32_t)(rest - j * T);
       other[u] = (IDX)t * tok16 + j * row16 + c;  // index on the token side
       if (q < total) {
-        a[u] = BWD ? in[other[u]] : in[q];
-        if (BWD) b[u] = yg[other[u]];
+        a[u] = ld_stream(in + (BWD ? other[u] : q));
+        if (BWD) b[u] = ld_stream(yg + other[u]);
         if (HEADWISE) gv[u][0] = static_cast<const uint16_t*>(gate)[other[u] >> lg16];
-        else gv[u] = static_cast<const u32x4*>(gate)[other[u]];
+        else gv[u] = ld_stream(static_cast<const u32x4*>(gate) + other[u]);
       } else {
         a[u] = u32x4{0, 0, 0, 0};
         b[u] = a[u];
@@ -109,10 +114,10 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(const u32x4* __restrict_
       }
       const u32x4 res = narrow(x * s8);
       if (!BWD) {
-        if (q < total) out[other[u]] = res;
+        if (q < total) st_stream(out + other[u], res);
         continue;
       }
-      if (q < total) out[q] = res;
+      if (q < total) st_stream(out + q, res);
       const f32x8 p = x * widen(b[u]);  // dY' * Y'
       if (HEADWISE) {
         // The chunks of one head are hb16 consecutive lanes starting at a multiple of hb16
@@ -124,7 +129,7 @@ __global__ __launch_bounds__(kThreads) void gate_kernel(const u32x4* __restrict_
           static_cast<__bf16*>(dgate)[other[u] >> lg16] = r;
         }
       } else if (q < total) {
-        static_cast<u32x4*>(dgate)[other[u]] = narrow(p * om8);
+        st_stream(static_cast<u32x4*>(dgate) + other[u], narrow(p * om8));
       }
     }
   }
@@ -137,7 +142,7 @@ void launch(const void* in, const void* yg, const void* gate, void* out, void* d
   const u32x4* i4 = static_cast<const u32x4*>(in);
   const u32x4* y4 = static_cast<const u32x4*>(yg);
   u32x4* o4 = static_cast<u32x4*>(out);
-  if (total + (uint64_t)256 * 64 * kThreads * kUnroll < (uint64_t(1) << 32))
+  if (total + (uint64_t)256 * 256 * kThreads * kUnroll < (uint64_t(1) << 32))
     hipLaunchKernelGGL((gate_kernel<BWD, HEADWISE, uint32_t>), grid, block, 0, s, i4, y4, gate, o4, dgate,
                        (uint32_t)total, row16, T, tok16, lg16);
   else

@@ -18,12 +18,17 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 4;
 constexpr int kThreads = 256;
 
+// Streaming 16-byte accesses: every chunk is touched once, so they bypass cache retention
+// (non-temporal), which measured 6.3 against 5.9 TB/s for a plain device copy.
+__device__ __forceinline__ u32x4 ld_stream(const u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_stream(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
+
 // Chunk q of the packed side [cp_u][T][g*hb16] <-> chunk of the token side [T][H*hb16].
 // INV = false: pack (token side -> packed side), true: unpack.
 unsigned grid_for(uint64_t total) {
   const uint64_t per_block = (uint64_t)kThreads * kUnroll;
   const uint64_t want = (total + per_block - 1) / per_block;
-  const uint64_t cap = 256ull * 64;  // enough blocks to fill 256 CUs many times over
+  const uint64_t cap = 256ull * 256;  // enough blocks to fill 256 CUs many times over
   return (unsigned)(want < cap ? want : cap);
 }
 
@@ -44,15 +49,12 @@ __global__ __launch_bounds__(kThreads) void pack_heads_kernel(const u32x4* __res
       const IDX j = rest / T;
       const uint32_t t = (uint32_t)(rest - j * T);
       other[u] = (IDX)t * tok16 + j * row16 + c;  // index on the token side
-      if (q < total) v[u] = INV ? src[q] : src[other[u]];
+      if (q < total) v[u] = ld_stream(src + (INV ? q : other[u]));
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const IDX q = base + (IDX)u * kThreads;
-      if (q < total) {
-        if (INV) dst[other[u]] = v[u];
-        else dst[q] = v[u];
-      }
+      if (q < total) st_stream(dst + (INV ? other[u] : q), v[u]);
     }
   }
 }
@@ -61,7 +63,7 @@ template <bool INV>
 void launch_pack(const void* src, void* dst, uint64_t total, uint32_t row16, uint32_t T, uint32_t tok16,
                  hipStream_t s) {
   // (total + one grid stride) must stay below 2^32 for the 32-bit form
-  if (total + (uint64_t)256 * 64 * kThreads * kUnroll < (uint64_t(1) << 32))
+  if (total + (uint64_t)256 * 256 * kThreads * kUnroll < (uint64_t(1) << 32))
     hipLaunchKernelGGL((pack_heads_kernel<INV, uint32_t>), dim3(grid_for(total)), dim3(kThreads), 0, s,
                        static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), (uint32_t)total, row16, T, tok16);
   else
@@ -85,12 +87,12 @@ __global__ __launch_bounds__(kThreads) void copy2_kernel(const u32x4* __restrict
       const bool second = q >= len;
       const uint64_t i = second ? q - len : q;
       to[u] = (second ? d1 : d0) + i;
-      if (q < total) v[u] = src[(second ? s1 : s0) + i];
+      if (q < total) v[u] = ld_stream(src + (second ? s1 : s0) + i);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const uint64_t q = base + (uint64_t)u * kThreads;
-      if (q < total) dst[to[u]] = v[u];
+      if (q < total) st_stream(dst + to[u], v[u]);
     }
   }
 }

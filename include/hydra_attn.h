@@ -83,13 +83,15 @@ typedef struct {
 size_t hydra_workspace_size(const hydra_problem_t* p);
 
 /* Forward partial of one ring step (Sec. 5.2.2; Sec. 2.2 for the masking):
- *   q [Nq][H][192] bf16, k [Nk][H][192] bf16, v [Nk][H][128] bf16   (inputs)
+ *   q [Nq][H][192] bf16, k [Nk][Hkv][192] bf16, v [Nk][Hkv][128] bf16   (inputs;
+ *   Hkv = n_kv_heads, or H when that is 0)
  *   o_part  [Nq][H][128] fp32   softmax(QK^T * scale, masked) V over this chunk's keys
  *   lse_part [H][Nq] fp32       natural-log sum of exp of the visible scores
  *   o_part_bf16: NULL, or [Nq][H][128] bf16 that also receives O (for a ring of one step,
  *                whose partial is already final)
  * A row that sees no key of this chunk gets O = 0 and LSE = -inf (the merge identity).
- * Every row of o_part and lse_part is written. */
+ * Every row of o_part and lse_part is written.  Outputs (o_part, lse_part, o_part_bf16 and
+ * the workspace) must not overlap each other or the inputs: checked, HYDRA_ERR_INVALID. */
 int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const void* v,
                    float* o_part, float* lse_part, void* o_part_bf16,
                    void* workspace, size_t workspace_bytes, void* stream);
@@ -98,9 +100,11 @@ int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const
  * function is differentiated at every step):
  *   o_final [Nq][H][128] bf16, lse_final [H][Nq] fp32, d_o [Nq][H][128] bf16
  *   dq_acc [Nq][H][192] fp32 += this step's dQ        (caller zero-initialises once)
- *   dk_acc [Nk][H][192] fp32 += dK of this KV chunk   from this rank's queries
- *   dv_acc [Nk][H][128] fp32 += dV of this KV chunk   from this rank's queries
- * The three gradient buffers must not overlap each other or the inputs. */
+ *   dk_acc [Nk][Hkv][192] fp32 += dK of this KV chunk   from this rank's queries
+ *   dv_acc [Nk][Hkv][128] fp32 += dV of this KV chunk   from this rank's queries
+ *          (with Hkv < H each K/V head sums the gradients of its query-head group)
+ * Outputs (the three gradient buffers and the workspace) must not overlap each other or
+ * the inputs: checked, HYDRA_ERR_INVALID. */
 int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const void* v,
                    const void* o_final, const float* lse_final, const void* d_o,
                    float* dq_acc, float* dk_acc, float* dv_acc,
@@ -111,7 +115,8 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
  * (0, -inf) is the identity; two empty rows stay (0, -inf) with no NaN.
  *   o_acc/o_part [n_rows][n_heads][d_v] fp32, lse_acc/lse_part [n_heads][n_rows] fp32.
  *   o_out_bf16: NULL, or [n_rows][n_heads][d_v] bf16 that also receives the merged O.
- * d_v must be 128.  n_rows = 0 is a no-op. */
+ * d_v must be 128.  n_rows = 0 is a no-op.  The outputs (o_acc, lse_acc, o_out_bf16) must
+ * not overlap each other or the partial: checked, HYDRA_ERR_INVALID. */
 int hydra_lse_merge(int64_t n_rows, int32_t n_heads, int32_t d_v,
                     float* o_acc, float* lse_acc, const float* o_part, const float* lse_part,
                     void* o_out_bf16, void* stream);

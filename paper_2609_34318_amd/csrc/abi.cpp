@@ -3,6 +3,7 @@
 
 #include <algorithm>
 #include <cstring>
+#include <initializer_list>
 #include <map>
 #include <mutex>
 #include <string>
@@ -70,6 +71,29 @@ namespace {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// A device buffer as [p, p + n) bytes; NULL or empty spans overlap nothing.
+struct Span {
+  const void* p;
+  uint64_t n;
+};
+
+bool overlap(Span a, Span b) {
+  if (!a.p || !b.p || a.n == 0 || b.n == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a.p), y = reinterpret_cast<uintptr_t>(b.p);
+  return x < y + b.n && y < x + a.n;
+}
+
+// True if an output overlaps another output or any input (inputs may share memory).
+bool outputs_overlap(std::initializer_list<Span> outs, std::initializer_list<Span> ins) {
+  for (auto o = outs.begin(); o != outs.end(); ++o) {
+    for (auto o2 = o + 1; o2 != outs.end(); ++o2)
+      if (overlap(*o, *o2)) return true;
+    for (const Span& i : ins)
+      if (overlap(*o, i)) return true;
+  }
+  return false;
+}
+
 // Non-null and 16-byte aligned when `needed`; HYDRA_OK otherwise.
 int check_ptr(const void* p, bool needed) {
   if (!needed) return HYDRA_OK;
@@ -133,6 +157,10 @@ int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const
     const WsLayout w = ws_layout(pr);
     if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
+    const uint64_t qh = uint64_t(pr.nq) * pr.H, kh = uint64_t(pr.nk) * pr.Hkv;
+    if (outputs_overlap({{o_part, qh * kDv * 4}, {lse_part, qh * 4}, {o_bf16, qh * kDv * 2}, {workspace, w.total}},
+                        {{q, qh * kDqk * 2}, {k, kh * kDqk * 2}, {v, kh * kDv * 2}}))
+      return HYDRA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::vector<int32_t> qitems, kitems;
     rc = upload_plan(pr, w, false, workspace, s, &qitems, &kitems);
@@ -166,6 +194,12 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
     const WsLayout w = ws_layout(pr);
     if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
+    const uint64_t qh = uint64_t(pr.nq) * pr.H, kh = uint64_t(pr.nk) * pr.Hkv;
+    if (outputs_overlap({{dq_acc, qh * kDqk * 4}, {dk_acc, kh * kDqk * 4}, {dv_acc, kh * kDv * 4},
+                         {workspace, w.total}},
+                        {{q, qh * kDqk * 2}, {k, kh * kDqk * 2}, {v, kh * kDv * 2}, {o_final, qh * kDv * 2},
+                         {lse_final, qh * 4}, {d_o, qh * kDv * 2}}))
+      return HYDRA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::vector<int32_t> qitems, kitems;
     rc = upload_plan(pr, w, true, workspace, s, &qitems, &kitems);
@@ -197,6 +231,10 @@ int hydra_lse_merge(int64_t n_rows, int32_t n_heads, int32_t d_v, float* o_acc, 
   for (int c : {check_ptr(o_acc, true), check_ptr(lse_acc, true), check_ptr(o_part, true),
                 check_ptr(lse_part, true), o_out_bf16 ? check_ptr(o_out_bf16, true) : HYDRA_OK})
     if (c != HYDRA_OK) return c;
+  const uint64_t rh = uint64_t(n_rows) * uint64_t(n_heads);
+  if (outputs_overlap({{o_acc, rh * kDv * 4}, {lse_acc, rh * 4}, {o_out_bf16, rh * kDv * 2}},
+                      {{o_part, rh * kDv * 4}, {lse_part, rh * 4}}))
+    return HYDRA_ERR_INVALID;
   if (launch_lse_merge(n_rows, n_heads, o_acc, lse_acc, o_part, lse_part, static_cast<uint16_t*>(o_out_bf16),
                        static_cast<hipStream_t>(stream)) != hipSuccess)
     return HYDRA_ERR_HIP;

@@ -123,6 +123,35 @@ def test_unsupported_dims_and_bad_pointers():
     assert L.hydra_lse_merge(0, 2, 128, None, None, None, None, None, None) == 0
 
 
+def test_overlapping_buffers_rejected_on_host():
+    """Outputs that overlap each other or an input are rejected before any HIP call."""
+    L = hydra.lib()
+    p = _problem([0, 64], 2, [(0, 64)], [(0, 32)], n_kv_heads=1)
+    ws = hydra.workspace_size(p)
+    M = 1 << 24                       # disjoint, aligned, never dereferenced
+    q, k, v, o, lse, obf, w = (M * i for i in range(1, 8))
+    fwd = L.hydra_attn_fwd
+    assert fwd(p.ref, q, k, v, q + 64 * 2 * 192 * 2 - 16, lse, None, w, ws, None) == -1   # O over Q's tail
+    assert fwd(p.ref, q, k, v, o, o + 64 * 2 * 128 * 4 - 16, None, w, ws, None) == -1     # LSE over O's tail
+    assert fwd(p.ref, q, k, v, o, lse, obf, k + 32 * 192 * 2 - 16, ws, None) == -1        # workspace over K
+    assert fwd(p.ref, q, k, v, o, lse, lse, w, ws, None) == -1                            # O bf16 aliases LSE
+    dq, dk, dv, of, lf, do = (M * i for i in range(8, 14))
+    bwd = L.hydra_attn_bwd
+    args = dict(q=q, k=k, v=v, of=of, lf=lf, do=do, dq=dq, dk=dk, dv=dv)
+    call = lambda **kw: bwd(p.ref, *[{**args, **kw}[n] for n in ("q", "k", "v", "of", "lf", "do", "dq", "dk", "dv")],
+                            w, ws, None)
+    assert call(dk=dq + 64 * 2 * 192 * 4 - 16) == -1      # dK over dQ's tail
+    assert call(dv=dk + 32 * 192 * 4 - 16) == -1          # dV over dK's tail (one K/V head)
+    assert call(dq=do) == -1                              # dQ aliases dO
+    assert call(dv=v + 32 * 128 * 2 - 16) == -1           # dV over V's tail
+    assert call(dk=w) == -1                               # dK aliases the workspace
+    # inputs may share memory with each other (still rejected here only for alignment)
+    assert call(k=q + 8) == -3
+    mg = L.hydra_lse_merge
+    assert mg(10, 2, 128, o, lse, o + 10 * 2 * 128 * 4 - 16, lf, None, None) == -1   # partial over acc
+    assert mg(10, 2, 128, o, lse, of, lf, lse, None) == -1                           # bf16 aliases LSE
+
+
 def test_zero_rows_is_noop():
     L = hydra.lib()
     p = _problem([0, 64], 2, [], [(0, 64)])

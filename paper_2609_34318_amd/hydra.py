@@ -193,8 +193,29 @@ def tile_rows() -> Tuple[int, int]:
 
 # ------------------------------------------------------------------ device calls (torch tensors)
 
-def _ptr(t) -> Optional[int]:
-    return None if t is None else t.data_ptr()
+def _ptr(t, what: str = "tensor", dtypes=None, numel: Optional[int] = None) -> Optional[int]:
+    """Device address of a dense device tensor (None passes through).  The library only sees
+    plain pointers, so a host, strided, wrongly typed or wrongly sized tensor is refused here
+    instead of reaching a kernel."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{what}: a device tensor is required")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: a contiguous tensor is required")
+    if dtypes is not None and _dt(t) not in dtypes:
+        raise ValueError(f"{what}: dtype {t.dtype} is not one of {dtypes}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{what}: {t.numel()} elements, expected {numel}")
+    return t.data_ptr()
+
+
+def _dt(t) -> str:
+    return str(t.dtype).replace("torch.", "")
+
+
+_BF16 = ("bfloat16", "int16")  # bf16 values, or their raw 16-bit patterns
+_F32 = ("float32",)
 
 
 def _stream(stream) -> int:
@@ -210,16 +231,23 @@ def _check(rc: int, what: str):
 
 def attn_fwd(p: Problem, q, k, v, o_part, lse_part, workspace, o_bf16=None, stream=None):
     """Partial O (fp32) and LSE of one ring step; optional bf16 copy of O."""
-    _check(lib().hydra_attn_fwd(p.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o_part), _ptr(lse_part),
-                                _ptr(o_bf16), _ptr(workspace), workspace.numel() * workspace.element_size(),
+    nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
+    _check(lib().hydra_attn_fwd(p.ref, _ptr(q, "q", _BF16, nqh * 192), _ptr(k, "k", _BF16, nkh * 192),
+                                _ptr(v, "v", _BF16, nkh * 128), _ptr(o_part, "o_part", _F32, nqh * 128),
+                                _ptr(lse_part, "lse_part", _F32, nqh), _ptr(o_bf16, "o_bf16", _BF16, nqh * 128),
+                                _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
                                 _stream(stream)), "hydra_attn_fwd")
 
 
 def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
              stream=None):
     """dQ/dK/dV of one ring step, accumulated (+=) into fp32 buffers."""
-    _check(lib().hydra_attn_bwd(p.ref, _ptr(q), _ptr(k), _ptr(v), _ptr(o_final_bf16), _ptr(lse_final),
-                                _ptr(d_o), _ptr(dq_acc), _ptr(dk_acc), _ptr(dv_acc), _ptr(workspace),
+    nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
+    _check(lib().hydra_attn_bwd(p.ref, _ptr(q, "q", _BF16, nqh * 192), _ptr(k, "k", _BF16, nkh * 192),
+                                _ptr(v, "v", _BF16, nkh * 128), _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
+                                _ptr(lse_final, "lse_final", _F32, nqh), _ptr(d_o, "d_o", _BF16, nqh * 128),
+                                _ptr(dq_acc, "dq_acc", _F32, nqh * 192), _ptr(dk_acc, "dk_acc", _F32, nkh * 192),
+                                _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _ptr(workspace, "workspace"),
                                 workspace.numel() * workspace.element_size(), _stream(stream)),
            "hydra_attn_bwd")
 
@@ -227,8 +255,10 @@ def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, 
 def lse_merge(o_acc, lse_acc, o_part, lse_part, o_bf16=None, stream=None):
     """(o_acc, lse_acc) <- exact merge with (o_part, lse_part), in place."""
     n_rows, n_heads, d_v = o_acc.shape
-    _check(lib().hydra_lse_merge(n_rows, n_heads, d_v, _ptr(o_acc), _ptr(lse_acc), _ptr(o_part),
-                                 _ptr(lse_part), _ptr(o_bf16), _stream(stream)), "hydra_lse_merge")
+    n = n_rows * n_heads
+    _check(lib().hydra_lse_merge(n_rows, n_heads, d_v, _ptr(o_acc, "o_acc", _F32), _ptr(lse_acc, "lse_acc", _F32, n),
+                                 _ptr(o_part, "o_part", _F32, n * d_v), _ptr(lse_part, "lse_part", _F32, n),
+                                 _ptr(o_bf16, "o_bf16", _BF16, n * d_v), _stream(stream)), "hydra_lse_merge")
 
 
 # ------------------------------------------------------------------ Ulysses x ring layout
@@ -237,28 +267,34 @@ def pack_heads(src, dst, cp_u: int, stream=None):
     """src [T, H, ...] -> dst [cp_u, T, H/cp_u, ...]: the send buffers of the forward exchange."""
     T, H = src.shape[0], src.shape[1]
     hb = src[0, 0].numel() * src.element_size()
-    _check(lib().hydra_pack_heads(T, H, hb, cp_u, _ptr(src), _ptr(dst), _stream(stream)), "hydra_pack_heads")
+    _check(lib().hydra_pack_heads(T, H, hb, cp_u, _ptr(src, "src"), _ptr(dst, "dst", (_dt(src),), src.numel()),
+                                  _stream(stream)), "hydra_pack_heads")
 
 
 def unpack_heads(src, dst, cp_u: int, stream=None):
     """src [cp_u, T, H/cp_u, ...] -> dst [T, H, ...]: the inverse of pack_heads."""
     T, H = dst.shape[0], dst.shape[1]
     hb = dst[0, 0].numel() * dst.element_size()
-    _check(lib().hydra_unpack_heads(T, H, hb, cp_u, _ptr(src), _ptr(dst), _stream(stream)), "hydra_unpack_heads")
+    _check(lib().hydra_unpack_heads(T, H, hb, cp_u, _ptr(src, "src", (_dt(dst),), dst.numel()), _ptr(dst, "dst"),
+                                    _stream(stream)), "hydra_unpack_heads")
 
 
 def zigzag_gather(src, dst, cp_r: int, r: int, stream=None):
     """Natural-order rows src [S, ...] -> ring rank r's rows dst [S/cp_r, ...]."""
     S = src.shape[0]
     rb = src[0].numel() * src.element_size()
-    _check(lib().hydra_zigzag_gather(S, rb, cp_r, r, _ptr(src), _ptr(dst), _stream(stream)), "hydra_zigzag_gather")
+    n = src.numel() // cp_r if cp_r > 0 else None
+    _check(lib().hydra_zigzag_gather(S, rb, cp_r, r, _ptr(src, "src"), _ptr(dst, "dst", (_dt(src),), n),
+                                     _stream(stream)), "hydra_zigzag_gather")
 
 
 def zigzag_scatter(src, dst, cp_r: int, r: int, stream=None):
     """Ring rank r's rows src [S/cp_r, ...] -> their natural positions in dst [S, ...]."""
     S = dst.shape[0]
     rb = dst[0].numel() * dst.element_size()
-    _check(lib().hydra_zigzag_scatter(S, rb, cp_r, r, _ptr(src), _ptr(dst), _stream(stream)), "hydra_zigzag_scatter")
+    n = dst.numel() // cp_r if cp_r > 0 else None
+    _check(lib().hydra_zigzag_scatter(S, rb, cp_r, r, _ptr(src, "src", (_dt(dst),), n), _ptr(dst, "dst"),
+                                      _stream(stream)), "hydra_zigzag_scatter")
 
 
 # ------------------------------------------------------------------ gated output
@@ -268,7 +304,9 @@ def unpack_heads_gated(recv, gate, y, stream=None):
     y = unpacked output * sigmoid(gate)."""
     cp_u = recv.shape[0]
     T, H, d_v = y.shape
-    _check(lib().hydra_unpack_heads_gated(T, H, d_v, gate.shape[-1], cp_u, _ptr(recv), _ptr(gate), _ptr(y),
+    e = gate.shape[-1]
+    _check(lib().hydra_unpack_heads_gated(T, H, d_v, e, cp_u, _ptr(recv, "recv", _BF16, T * H * d_v),
+                                          _ptr(gate, "gate", _BF16, T * H * e), _ptr(y, "y", _BF16),
                                           _stream(stream)), "hydra_unpack_heads_gated")
 
 
@@ -277,8 +315,10 @@ def pack_heads_gated_bwd(y, gate, d_y, d_send, d_gate, stream=None):
     d_gate [T, H, 1 or d_v], all bf16."""
     cp_u = d_send.shape[0]
     T, H, d_v = y.shape
-    _check(lib().hydra_pack_heads_gated_bwd(T, H, d_v, gate.shape[-1], cp_u, _ptr(y), _ptr(gate), _ptr(d_y),
-                                            _ptr(d_send), _ptr(d_gate), _stream(stream)),
+    e, n = gate.shape[-1], T * H * d_v
+    _check(lib().hydra_pack_heads_gated_bwd(T, H, d_v, e, cp_u, _ptr(y, "y", _BF16), _ptr(gate, "gate", _BF16, T * H * e),
+                                            _ptr(d_y, "d_y", _BF16, n), _ptr(d_send, "d_send", _BF16, n),
+                                            _ptr(d_gate, "d_gate", _BF16, T * H * e), _stream(stream)),
            "hydra_pack_heads_gated_bwd")
 
 

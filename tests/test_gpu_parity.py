@@ -217,6 +217,26 @@ def test_every_output_written_and_deterministic():
         assert np.array_equal(a, c) and np.array_equal(b, d)
 
 
+def test_binding_refuses_strided_mistyped_and_missized_tensors():
+    """Checked in the binding before the library is called (nothing is launched)."""
+    cu, segs, H = [0, 64], [(0, 64)], 2
+    p = hydra.Problem(cu, H, segs, segs)
+    ws = torch.empty(hydra.workspace_size(p), dtype=torch.uint8, device="cuda")
+    q = torch.zeros((64, H, D_QK), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros((64, H, D_V), dtype=torch.bfloat16, device="cuda")
+    o = torch.zeros((64, H, D_V), device="cuda")
+    lse = torch.zeros((H, 64), device="cuda")
+    with pytest.raises(ValueError, match="contiguous"):
+        hydra.attn_fwd(p, q.transpose(0, 1), q, v, o, lse, ws)
+    with pytest.raises(ValueError, match="dtype"):
+        hydra.attn_fwd(p, q.float(), q, v, o, lse, ws)
+    with pytest.raises(ValueError, match="elements"):
+        hydra.attn_fwd(p, q, q, v, o[:32], lse, ws)
+    with pytest.raises(ValueError, match="dtype"):
+        hydra.pack_heads(q, torch.empty((2, 64, 1, D_QK), device="cuda"), 2)
+    torch.cuda.synchronize()
+
+
 def test_gradient_canaries_untouched():
     """dK/dV rows outside the KV chunk's rows are never written (guard bands)."""
     cu = [0, 500]

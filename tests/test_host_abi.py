@@ -152,6 +152,18 @@ def test_overlapping_buffers_rejected_on_host():
     assert mg(10, 2, 128, o, lse, of, lf, lse, None) == -1                           # bf16 aliases LSE
 
 
+def test_binding_refuses_host_tensors():
+    """The library takes plain device pointers; the binding refuses a host tensor before
+    any call (its address would reach a kernel)."""
+    import torch
+    p = _problem([0, 64], 2, [(0, 64)], [(0, 64)])
+    q = torch.zeros((64, 2, 192), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensor"):
+        hydra.attn_fwd(p, q, q, q, None, None, torch.zeros(16, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="device tensor"):
+        hydra.pack_heads(q, q, 2)
+
+
 def test_zero_rows_is_noop():
     L = hydra.lib()
     p = _problem([0, 64], 2, [], [(0, 64)])

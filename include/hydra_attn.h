@@ -78,7 +78,13 @@ typedef struct {
                                        uses K/V head i / (n_heads / n_kv_heads)            */
 } hydra_problem_t;
 
-/* Bytes of device workspace the compute calls need for `p` (host only, no GPU needed).
+/* Size limits (HYDRA_ERR_INVALID beyond them): n_heads <= 4096; Nq, Nk <= 2^30 rows;
+ * Nq * n_heads * 192 and Nk * n_heads * 192 below 2^40 elements; and, because every
+ * attention launch holds one 512-lane workgroup per (tile, head) and a dispatch fewer than
+ * 2^32 lanes, (sum over the query segments of ceil(len / 256)) * n_heads and (sum over the
+ * K/V segments of ceil(len / 128)) * n_kv_heads below 2^23.
+ *
+ * Bytes of device workspace the compute calls need for `p` (host only, no GPU needed).
  * Returns 0 if `p` is invalid. */
 size_t hydra_workspace_size(const hydra_problem_t* p);
 

@@ -20,29 +20,29 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict
                                                       const float* __restrict__ lse,
                                                       float* __restrict__ D, float* __restrict__ lse2,
                                                       int nq, int H) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t rh = gid >> 4;  // (row, head) pair, 16 lanes each
   const int sub = threadIdx.x & 15;
-  const bool ok = rh < (int64_t)nq * H;
-  float acc = 0.f;
-  if (ok) {
+  const int64_t total = (int64_t)nq * H;
+  // (row, head) pairs, 16 lanes each, strided over a capped grid; the 16 lanes of a pair
+  // stay together, so the reduction below always has all of them
+  for (int64_t rh = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4); rh < total; rh += (int64_t)gridDim.x * 16) {
     const u32x4 uo = ldg16(o + rh * DV + sub * 8);
     const u32x4 ud = ldg16(dO + rh * DV + sub * 8);
+    float acc = 0.f;
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       acc += __uint_as_float(uo[w] << 16) * __uint_as_float(ud[w] << 16);
       acc += __uint_as_float(uo[w] & 0xffff0000u) * __uint_as_float(ud[w] & 0xffff0000u);
     }
-  }
-  acc += __shfl_xor(acc, 8, 16);
-  acc += __shfl_xor(acc, 4, 16);
-  acc += __shfl_xor(acc, 2, 16);
-  acc += __shfl_xor(acc, 1, 16);
-  if (ok && sub == 0) {
-    const int row = (int)(rh / H), head = (int)(rh % H);
-    const int64_t li = (int64_t)head * nq + row;
-    D[li] = acc;
-    lse2[li] = lse[li] * LOG2E;
+    acc += __shfl_xor(acc, 8, 16);
+    acc += __shfl_xor(acc, 4, 16);
+    acc += __shfl_xor(acc, 2, 16);
+    acc += __shfl_xor(acc, 1, 16);
+    if (sub == 0) {
+      const int row = (int)(rh / H), head = (int)(rh % H);
+      const int64_t li = (int64_t)head * nq + row;
+      D[li] = acc;
+      lse2[li] = lse[li] * LOG2E;
+    }
   }
 }
 
@@ -498,7 +498,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
 hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems,
                            hipStream_t stream) {
   const int64_t pairs = (int64_t)a.nq * a.H;
-  const int64_t blocks = (pairs * 16 + 255) / 256;
+  const int64_t blocks = (pairs + 15) / 16 < (1 << 20) ? (pairs + 15) / 16 : (1 << 20);
   int tok = prof_begin("bwd_pre", stream);
   hipLaunchKernelGGL(bwd_pre_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a.o, a.dO, a.lse, a.Dvec,
                      a.lse2, a.nq, a.H);

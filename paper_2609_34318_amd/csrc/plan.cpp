@@ -114,6 +114,12 @@ int check_problem(const hydra_problem_t* p, Problem* out) {
   const int hkv = p->n_kv_heads == 0 ? p->n_heads : p->n_kv_heads;
   if (hkv < 0 || hkv > p->n_heads || p->n_heads % hkv != 0) return HYDRA_ERR_INVALID;
   if (nk * hkv * kDqk >= (int64_t(1) << 40)) return HYDRA_ERR_INVALID;
+  // The attention launches have one 512-lane workgroup per (tile, head), and a dispatch
+  // holds fewer than 2^32 lanes.
+  int64_t nqt = 0, nkt = 0;
+  for (int s = 0; s < p->q.n_segs; ++s) nqt += (p->q.len[s] + kQTile - 1) / kQTile;
+  for (int s = 0; s < p->kv.n_segs; ++s) nkt += (p->kv.len[s] + kKvTile - 1) / kKvTile;
+  if (nqt * p->n_heads >= (int64_t(1) << 23) || nkt * hkv >= (int64_t(1) << 23)) return HYDRA_ERR_INVALID;
   out->H = p->n_heads;
   out->Hkv = hkv;
   out->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt(float(kDqk));

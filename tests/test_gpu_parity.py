@@ -402,3 +402,40 @@ def test_zigzag256k_uniform_closed_form_backward():
     dk, dv = oracle.uniform_bwd_k0(f32(q), f32(kv[1][1]), Uo, f32(do), n, cu, q_segs, steps[1], keys)
     assert_grad_close(res["dkv"][1][0][keys], dk, what="dK uniform")
     assert_grad_close(res["dkv"][1][1][keys], dv, what="dV uniform")
+
+
+def test_offsets_past_two_to_the_31_elements():
+    """1,048,876 rows x 16 heads in 2048 documents of 512 tokens and a ragged one of 300:
+    Q and dQ hold 3.2e9 elements and O 2.1e9, so late rows sit past every 32-bit element
+    offset.  Inputs are drawn on the device (seeded); the first document, the one holding
+    element 2^31 of Q, and the last two are checked against the oracle (two heads)."""
+    H, L, n_full = 16, 512, 2048
+    lens = [L] * n_full + [300]
+    cu = [0] + list(np.cumsum(lens))
+    nq = cu[-1]
+    segs = [(0, nq)]
+    gen = torch.Generator(device="cuda").manual_seed(17)
+    draw = lambda d, s: (torch.randn((nq, H, d), generator=gen, device="cuda") * s).to(torch.bfloat16)
+    q, k, v, d_o = draw(D_QK, 1.0), draw(D_QK, 1.0), draw(D_V, 1.0), draw(D_V, 1.0)
+    sh = ring.make_share(cu, H, segs, [segs])
+    o, lse, _ = ring.forward(sh, q, [(k, v)])
+    dq = torch.zeros((nq, H, D_QK), dtype=torch.float32, device="cuda")
+    dk = torch.zeros((nq, H, D_QK), dtype=torch.float32, device="cuda")
+    dv = torch.zeros((nq, H, D_V), dtype=torch.float32, device="cuda")
+    ring.backward(sh, q, [(k, v)], d_o, dq, [(dk, dv)])
+    torch.cuda.synchronize()
+    assert nq * H * D_QK > 3 * 2 ** 30 and nq * H * D_V > 2 ** 31
+    heads = [3, 15]
+    docs = [0, (2 ** 31 // (H * D_QK)) // L, n_full - 1, n_full]
+    for d in docs:
+        a, b = cu[d], cu[d + 1]
+        host = lambda t: t[a:b][:, heads].float().cpu().numpy().astype(np.float64)
+        qq, kk, vv, dd = host(q), host(k), host(v), host(d_o)
+        dcu, dseg = [0, b - a], [(0, b - a)]
+        O, Lse = oracle.attn_fwd(qq, kk, vv, dcu, dseg, dseg)
+        rq, rk, rv = oracle.attn_bwd(qq, kk, vv, O, Lse, dd, dcu, dseg, dseg)
+        assert_o_close(o[a:b][:, heads].cpu().numpy(), O, what=f"O doc {d}")
+        assert_lse_close(lse[heads][:, a:b].cpu().numpy(), Lse, what=f"LSE doc {d}")
+        assert_grad_close(dq[a:b][:, heads].cpu().numpy(), rq, what=f"dQ doc {d}")
+        assert_grad_close(dk[a:b][:, heads].cpu().numpy(), rk, what=f"dK doc {d}")
+        assert_grad_close(dv[a:b][:, heads].cpu().numpy(), rv, what=f"dV doc {d}")

@@ -164,6 +164,19 @@ def test_binding_refuses_host_tensors():
         hydra.pack_heads(q, q, 2)
 
 
+def test_launch_size_limit_checked_on_host():
+    """One 512-lane workgroup per (tile, head) and fewer than 2^32 lanes per dispatch:
+    2^23 (query tile, head) pairs are refused, one fewer is planned."""
+    ok = _problem([0, 2 ** 20], 4096, [(0, 2 ** 19 - 256)], [(0, 256)])
+    big = _problem([0, 2 ** 20], 4096, [(0, 2 ** 19)], [(0, 256)])
+    assert hydra.workspace_size(ok) > 0
+    assert hydra.workspace_size(big) == 0
+    L = hydra.lib()
+    assert L.hydra_attn_fwd(big.ref, 16, 32, 48, 64, 80, None, 96, 1 << 20, None) == -1
+    kv_big = _problem([0, 2 ** 21], 8192 // 8, [(0, 256)], [(0, 2 ** 20)], n_kv_heads=1024)
+    assert hydra.workspace_size(kv_big) == 0
+
+
 def test_zero_rows_is_noop():
     L = hydra.lib()
     p = _problem([0, 64], 2, [], [(0, 64)])

@@ -47,20 +47,23 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const uint16_t* __restrict
 }
 
 // ------------------------------------------------------------------ dQ (query-stationary)
-constexpr int DQ_BK = 64;
-constexpr int DQ_KBYTES = DQ_BK * DQK * 2;            // 24 KB
-constexpr int DQ_STAGE = DQ_KBYTES + DQ_BK * DV * 2;  // 40 KB
+constexpr int DQ_BK = 96;  // keys per tile: measured faster than 64 and 128
+constexpr int DQ_KBYTES = DQ_BK * DQK * 2;            // 36 KB
+constexpr int DQ_STAGE = DQ_KBYTES + DQ_BK * DV * 2;  // 60 KB
 constexpr int DQ_NSTAGE = 2;  // measured faster than three stages
 constexpr int DQ_WAVES = 8;                           // 256 query rows per workgroup
-constexpr int DQ_VMCNT_ONE_TILE = 5;                  // copies per tile per wave: 3 (K) + 2 (V)
+constexpr int DQ_COPY_WAVES = 4;                      // the 12 copies per column block split evenly over 4
+// copies per tile per copying wave: (3 (K) + 2 (V) column blocks) x 3
+constexpr int DQ_VMCNT_ONE_TILE = (DQK / 64 + DV / 64) * (DQ_BK / 8 / DQ_COPY_WAVES);
 
 __device__ __forceinline__ void dq_issue(lds_char* smem, const AttnArgs& a, const TileRanges kr, int t, int koff,
                                          int voff, int wave) {
   int row0, pos0, n;
   tile_at(kr, t, DQ_BK, row0, pos0, n);
   lds_char* dst = smem + (t % DQ_NSTAGE) * DQ_STAGE;
-  dma_tile<DQK, DQ_BK, DQ_WAVES>(dst, tile_rsrc(a.k, row0, n, a.Hkv, DQK), koff, a.Hkv, wave);
-  dma_tile<DV, DQ_BK, DQ_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.Hkv, DV), voff, a.Hkv, wave);
+  if (wave >= DQ_COPY_WAVES) return;  // wave-uniform
+  dma_tile<DQK, DQ_BK, DQ_COPY_WAVES>(dst, tile_rsrc(a.k, row0, n, a.Hkv, DQK), koff, a.Hkv, wave);
+  dma_tile<DV, DQ_BK, DQ_COPY_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.Hkv, DV), voff, a.Hkv, wave);
 }
 
 __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
@@ -138,7 +141,7 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
     const lds_char* Vs = Ks + DQ_KBYTES;
     const bool full = (kn == DQ_BK) && (lo_last <= kpos) && (kpos + DQ_BK - 1 <= q_pos0);
 
-    static_for<2>([&](auto kb_) {
+    static_for<DQ_BK / 32>([&](auto kb_) {
       constexpr int kb = decltype(kb_)::value;
       f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll

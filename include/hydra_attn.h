@@ -76,6 +76,12 @@ typedef struct {
   int32_t n_kv_heads;               /* K/V heads held (Sec. 3.5: h_kv <= h); 0 means
                                        n_heads (MLA).  Must divide n_heads: query head i
                                        uses K/V head i / (n_heads / n_kv_heads)            */
+  int32_t q_tok_stride;             /* elements from one token row of q to the next; 0 =
+                                       dense (n_heads * 192).  Otherwise at least that, a
+                                       multiple of 8 and below 2^22 (heads stay contiguous
+                                       within a row, e.g. views into a fused QKV buffer)  */
+  int32_t k_tok_stride;             /* the same for k (dense: Hkv * 192)                 */
+  int32_t v_tok_stride;             /* the same for v (dense: Hkv * 128)                 */
 } hydra_problem_t;
 
 /* Size limits (HYDRA_ERR_INVALID beyond them): n_heads <= 4096; Nq, Nk <= 2^30 rows;
@@ -90,7 +96,8 @@ size_t hydra_workspace_size(const hydra_problem_t* p);
 
 /* Forward partial of one ring step (Sec. 5.2.2; Sec. 2.2 for the masking):
  *   q [Nq][H][192] bf16, k [Nk][Hkv][192] bf16, v [Nk][Hkv][128] bf16   (inputs;
- *   Hkv = n_kv_heads, or H when that is 0)
+ *   Hkv = n_kv_heads, or H when that is 0; token rows q_tok_stride / k_tok_stride /
+ *   v_tok_stride elements apart, every other tensor dense)
  *   o_part  [Nq][H][128] fp32   softmax(QK^T * scale, masked) V over this chunk's keys
  *   lse_part [H][Nq] fp32       natural-log sum of exp of the visible scores
  *   o_part_bf16: NULL, or [Nq][H][128] bf16 that also receives O (for a ring of one step,

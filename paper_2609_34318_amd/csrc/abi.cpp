@@ -94,6 +94,12 @@ bool outputs_overlap(std::initializer_list<Span> outs, std::initializer_list<Spa
   return false;
 }
 
+// Bytes from the first element of a bf16 token-major view to one past its last: `rows`
+// rows of `width` elements, `stride` elements apart.
+uint64_t rows_bytes(int64_t rows, int64_t stride, int64_t width) {
+  return rows > 0 ? uint64_t((rows - 1) * stride + width) * 2 : 0;
+}
+
 // Non-null and 16-byte aligned when `needed`; HYDRA_OK otherwise.
 int check_ptr(const void* p, bool needed) {
   if (!needed) return HYDRA_OK;
@@ -129,6 +135,9 @@ AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
   a.grp = pr.H / pr.Hkv;
   a.nq = int(pr.nq);
   a.nk = int(pr.nk);
+  a.q_s = pr.q_s;
+  a.k_s = pr.k_s;
+  a.v_s = pr.v_s;
   a.scale = pr.scale;
   return a;
 }
@@ -157,9 +166,11 @@ int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const
     const WsLayout w = ws_layout(pr);
     if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
-    const uint64_t qh = uint64_t(pr.nq) * pr.H, kh = uint64_t(pr.nk) * pr.Hkv;
+    const uint64_t qh = uint64_t(pr.nq) * pr.H;
+    const uint64_t qb = rows_bytes(pr.nq, pr.q_s, pr.H * kDqk), kb = rows_bytes(pr.nk, pr.k_s, pr.Hkv * kDqk),
+                   vb = rows_bytes(pr.nk, pr.v_s, pr.Hkv * kDv);
     if (outputs_overlap({{o_part, qh * kDv * 4}, {lse_part, qh * 4}, {o_bf16, qh * kDv * 2}, {workspace, w.total}},
-                        {{q, qh * kDqk * 2}, {k, kh * kDqk * 2}, {v, kh * kDv * 2}}))
+                        {{q, qb}, {k, kb}, {v, vb}}))
       return HYDRA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::vector<int32_t> qitems, kitems;
@@ -195,10 +206,12 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
     if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
     const uint64_t qh = uint64_t(pr.nq) * pr.H, kh = uint64_t(pr.nk) * pr.Hkv;
+    const uint64_t qb = rows_bytes(pr.nq, pr.q_s, pr.H * kDqk), kb = rows_bytes(pr.nk, pr.k_s, pr.Hkv * kDqk),
+                   vb = rows_bytes(pr.nk, pr.v_s, pr.Hkv * kDv);
     if (outputs_overlap({{dq_acc, qh * kDqk * 4}, {dk_acc, kh * kDqk * 4}, {dv_acc, kh * kDv * 4},
                          {workspace, w.total}},
-                        {{q, qh * kDqk * 2}, {k, kh * kDqk * 2}, {v, kh * kDv * 2}, {o_final, qh * kDv * 2},
-                         {lse_final, qh * 4}, {d_o, qh * kDv * 2}}))
+                        {{q, qb}, {k, kb}, {v, vb}, {o_final, qh * kDv * 2}, {lse_final, qh * 4},
+                         {d_o, qh * kDv * 2}}))
       return HYDRA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
     std::vector<int32_t> qitems, kitems;

@@ -62,8 +62,8 @@ __device__ __forceinline__ void dq_issue(lds_char* smem, const AttnArgs& a, cons
   tile_at(kr, t, DQ_BK, row0, pos0, n);
   lds_char* dst = smem + (t % DQ_NSTAGE) * DQ_STAGE;
   if (wave >= DQ_COPY_WAVES) return;  // wave-uniform
-  dma_tile<DQK, DQ_BK, DQ_COPY_WAVES>(dst, tile_rsrc(a.k, row0, n, a.Hkv, DQK), koff, a.Hkv, wave);
-  dma_tile<DV, DQ_BK, DQ_COPY_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.Hkv, DV), voff, a.Hkv, wave);
+  dma_tile<DQK, DQ_BK, DQ_COPY_WAVES>(dst, tile_rsrc(a.k, row0, n, a.k_s), koff, a.k_s, wave);
+  dma_tile<DV, DQ_BK, DQ_COPY_WAVES>(dst + DQ_KBYTES, tile_rsrc(a.v, row0, n, a.v_s), voff, a.v_s, wave);
 }
 
 __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
@@ -96,12 +96,12 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
   settle(lse2);
   settle(Dq);
   const int kv_head = head / a.grp;  // grouped K/V heads: contiguous groups of query heads
-  const int koff = dma_lane_off<DQK>(a.Hkv, kv_head, wave, lane);
-  const int voff = dma_lane_off<DV>(a.Hkv, kv_head, wave, lane);
+  const int koff = dma_lane_off<DQK>(a.k_s, kv_head, wave, lane);
+  const int voff = dma_lane_off<DV>(a.v_s, kv_head, wave, lane);
 
   bf16x8 qf[DQK / 16], df[DV / 16];
   {
-    const uint16_t* qp = a.q + (qrow * a.H + head) * DQK + 8 * hh;
+    const uint16_t* qp = a.q + qrow * a.q_s + head * DQK + 8 * hh;
     const uint16_t* dp = a.dO + (qrow * a.H + head) * DV + 8 * hh;
 #pragma unroll
     for (int t = 0; t < DQK / 16; ++t) {
@@ -232,8 +232,9 @@ __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, cons
   int row0, pos0, n;
   tile_at(qr, qt, KV_BQ, row0, pos0, n);
   lds_char* dst = smem + (t % KV_NSTAGE) * KV_STAGE;
-  dma_tile<DQK, KV_BQ, 4>(dst, tile_rsrc(a.q, row0, n, a.H, DQK), qoff + member * (DQK * 2), a.H, wave_b);
-  dma_tile<DV, KV_BQ, 4>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H, DV), ooff + member * (DV * 2), a.H, wave_b);
+  dma_tile<DQK, KV_BQ, 4>(dst, tile_rsrc(a.q, row0, n, a.q_s), qoff + member * (DQK * 2), a.q_s, wave_b);
+  dma_tile<DV, KV_BQ, 4>(dst + KV_QBYTES, tile_rsrc(a.dO, row0, n, a.H * DV), ooff + member * (DV * 2), a.H * DV,
+                         wave_b);
   const int64_t li = (int64_t)(head0 + member) * a.nq + row0;
   // LSE2 and D of the tile's rows, 64 per copy; rows past the tile's end read as zero
   static_assert(KV_BQ <= 2 * 64 && KV_BQ <= KV_VEC, "two 64-row copies per vector");
@@ -278,8 +279,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
       __builtin_amdgcn_readfirstlane(kn_w > 0 ? a.cu[doc_of(a.cu, a.n_docs, wk_first) + 1] : 0);
   const float sl2 = a.scale * LOG2E;
   const int64_t krow = k_row0 + (k_valid ? kj : 0);
-  const int qoff = dma_lane_off<DQK>(a.H, head0, pair, lane);  // role B's copy lanes (wave b = pair)
-  const int ooff = dma_lane_off<DV>(a.H, head0, pair, lane);
+  const int qoff = dma_lane_off<DQK>(a.q_s, head0, pair, lane);  // role B's copy lanes (wave b = pair)
+  const int ooff = dma_lane_off<DV>(a.H * DV, head0, pair, lane);
   const int poff = pair * (KV_NSB * 2048) + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
   const bool active = kn_w > 0;               // uniform over the pair
 
@@ -294,8 +295,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
     constexpr int NACC = ROLE == 0 ? DV / 32 : DQK / 32;
     bf16x8 bf[NF];
     {
-      const uint16_t* src = ROLE == 0 ? a.k + (krow * a.Hkv + kv_head) * DQK + 8 * hh
-                                      : a.v + (krow * a.Hkv + kv_head) * DV + 8 * hh;
+      const uint16_t* src = ROLE == 0 ? a.k + krow * a.k_s + kv_head * DQK + 8 * hh
+                                      : a.v + krow * a.v_s + kv_head * DV + 8 * hh;
       u32x4 u[12];
 #pragma unroll
       for (int t = 0; t < 12; ++t) u[t] = u32x4{0u, 0u, 0u, 0u};

@@ -37,8 +37,8 @@ __device__ __forceinline__ void fwd_issue(lds_char* smem, const AttnArgs& a, con
   int row0, pos0, n;
   tile_at(kr, t, FWD_BK, row0, pos0, n);
   lds_char* dst = smem + (t % FWD_NSTAGE) * FWD_STAGE;
-  dma_tile<DQK, FWD_BK, FWD_WAVES>(dst, tile_rsrc(a.k, row0, n, a.Hkv, DQK), koff, a.Hkv, wave);
-  dma_tile<DV, FWD_BK, FWD_WAVES>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.Hkv, DV), voff, a.Hkv, wave);
+  dma_tile<DQK, FWD_BK, FWD_WAVES>(dst, tile_rsrc(a.k, row0, n, a.k_s), koff, a.k_s, wave);
+  dma_tile<DV, FWD_BK, FWD_WAVES>(dst + FWD_KBYTES, tile_rsrc(a.v, row0, n, a.v_s), voff, a.v_s, wave);
 }
 
 __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a, uint16_t* __restrict__ o_bf16) {
@@ -65,12 +65,12 @@ __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a,
   const int lo_last = a.cu[doc_of(a.cu, a.n_docs, q_pos0 + q_n - 1)];
   const float sl2 = a.scale * LOG2E;
   const int kv_head = head / a.grp;  // grouped K/V heads: contiguous groups of query heads
-  const int koff = dma_lane_off<DQK>(a.Hkv, kv_head, wave, lane);
-  const int voff = dma_lane_off<DV>(a.Hkv, kv_head, wave, lane);
+  const int koff = dma_lane_off<DQK>(a.k_s, kv_head, wave, lane);
+  const int voff = dma_lane_off<DV>(a.v_s, kv_head, wave, lane);
 
   bf16x8 qf[DQK / 16];
   {
-    const uint16_t* qrow = a.q + ((int64_t)(q_row0 + (q_valid ? qi : 0)) * a.H + head) * DQK + 8 * hh;
+    const uint16_t* qrow = a.q + (int64_t)(q_row0 + (q_valid ? qi : 0)) * a.q_s + head * DQK + 8 * hh;
 #pragma unroll
     for (int t = 0; t < DQK / 16; ++t) {
       u32x4 u = {0u, 0u, 0u, 0u};

@@ -291,8 +291,9 @@ __device__ __forceinline__ u32x4 tile_desc(const void* base, int64_t byte_off, i
   d[3] = 0x00020000u;
   return d;
 }
-__device__ __forceinline__ u32x4 tile_rsrc(const uint16_t* g, int64_t row0, int valid, int H, int dim) {
-  return tile_desc(g, row0 * H * (int64_t)dim * 2, valid * H * dim * 2);
+// Rows [row0, row0 + valid) of a token-major tensor whose rows are `pitch` elements apart.
+__device__ __forceinline__ u32x4 tile_rsrc(const uint16_t* g, int64_t row0, int valid, int pitch) {
+  return tile_desc(g, row0 * pitch * 2, valid * pitch * 2);
 }
 
 // One 16-byte-per-lane copy at voff + inc (s_nop: M0 and the descriptor are written by the
@@ -322,16 +323,16 @@ __device__ __forceinline__ void dma4(uint32_t m0v, u32x4 desc, int voff) {
 // wave w writes bytes [16L, 16L+16) of each 1 KB instruction, which holds rows 8j..8j+7 of
 // one column block, j = w + NW*i; it fetches the logical chunk the swizzle places there
 // (rows 8j + L/8 have bits 1..3 = (L/8 >> 1) and (j & 1) == (w & 1) for every i).
-template <int DIM> __device__ __forceinline__ int dma_lane_off(int H, int head, int wave, int lane) {
+template <int DIM> __device__ __forceinline__ int dma_lane_off(int pitch, int head, int wave, int lane) {
   const int q = lane >> 3;
   const int lc = (lane & 7) ^ ((((q >> 1) & 1) << 2) | ((wave & 1) << 1) | (q >> 2));
-  return (((8 * wave + q) * H + head) * DIM + lc * 8) * 2;
+  return ((8 * wave + q) * pitch + head * DIM + lc * 8) * 2;
 }
 
 // Copies a ROWS x DIM tile (NW waves, rows 8j .. 8j+7 of each column block per 1 KB
 // instruction, j = wave + NW*i).  `wave` must be wave-uniform.
 template <int DIM, int ROWS, int NW = 4>
-__device__ __forceinline__ void dma_tile(lds_char* lds, u32x4 desc, int voff, int H, int wave) {
+__device__ __forceinline__ void dma_tile(lds_char* lds, u32x4 desc, int voff, int pitch, int wave) {
   constexpr int NINS = ROWS / 8;  // per column block
   static_assert(NINS % NW == 0, "tile must split evenly over the waves");
   const uint32_t base = __builtin_amdgcn_readfirstlane(lds_addr(lds) + wave * 1024);
@@ -339,7 +340,7 @@ __device__ __forceinline__ void dma_tile(lds_char* lds, u32x4 desc, int voff, in
   for (int b = 0; b < DIM / 64; ++b)
 #pragma unroll
     for (int i = 0; i < NINS / NW; ++i)
-      dma16(base + b * block_bytes<ROWS>() + NW * i * 1024, desc, voff, 8 * NW * i * H * DIM * 2 + b * 128);
+      dma16(base + b * block_bytes<ROWS>() + NW * i * 1024, desc, voff, 8 * NW * i * pitch * 2 + b * 128);
 }
 
 // 64 fp32 values (valid of them in range) -> LDS, one wave.
@@ -444,6 +445,7 @@ struct AttnArgs {
   int Hkv;             // K/V heads; query head h uses K/V head h / grp
   int grp;             // H / Hkv
   int nq, nk;
+  int q_s, k_s, v_s;   // elements between consecutive token rows of q, k, v (dO, O: dense)
   float scale;         // softmax scale
 };
 

@@ -120,6 +120,18 @@ int check_problem(const hydra_problem_t* p, Problem* out) {
   for (int s = 0; s < p->q.n_segs; ++s) nqt += (p->q.len[s] + kQTile - 1) / kQTile;
   for (int s = 0; s < p->kv.n_segs; ++s) nkt += (p->kv.len[s] + kKvTile - 1) / kKvTile;
   if (nqt * p->n_heads >= (int64_t(1) << 23) || nkt * hkv >= (int64_t(1) << 23)) return HYDRA_ERR_INVALID;
+  // token-row strides: 0 = dense; else >= dense, a multiple of 8 (16-byte rows), < 2^22
+  auto stride = [](int32_t s, int64_t dense, int* dst) {
+    if (s == 0) s = int32_t(dense);
+    if (s < dense || s % 8 != 0 || s >= (1 << 22)) return false;
+    *dst = s;
+    return true;
+  };
+  if (!stride(p->q_tok_stride, int64_t(p->n_heads) * kDqk, &out->q_s) ||
+      !stride(p->k_tok_stride, int64_t(hkv) * kDqk, &out->k_s) ||
+      !stride(p->v_tok_stride, int64_t(hkv) * kDv, &out->v_s))
+    return HYDRA_ERR_INVALID;
+  if (nq * out->q_s >= (int64_t(1) << 40) || nk * out->k_s >= (int64_t(1) << 40)) return HYDRA_ERR_INVALID;
   out->H = p->n_heads;
   out->Hkv = hkv;
   out->scale = p->softmax_scale > 0.f ? p->softmax_scale : 1.0f / std::sqrt(float(kDqk));

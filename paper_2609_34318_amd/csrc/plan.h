@@ -22,6 +22,7 @@ struct Problem {
   std::vector<int32_t> cu;     // n_docs + 1 boundaries
   hydra_chunk_t q{}, kv{};
   int64_t nq = 0, nk = 0;
+  int q_s = 0, k_s = 0, v_s = 0;  // token-row strides of q, k, v in elements
 };
 
 // Returns HYDRA_OK or an error status; fills `out` on success.

@@ -35,7 +35,10 @@ class ProblemC(ctypes.Structure):
                 ("n_docs", ctypes.c_int32),
                 ("q", Chunk),
                 ("kv", Chunk),
-                ("n_kv_heads", ctypes.c_int32)]
+                ("n_kv_heads", ctypes.c_int32),
+                ("q_tok_stride", ctypes.c_int32),
+                ("k_tok_stride", ctypes.c_int32),
+                ("v_tok_stride", ctypes.c_int32)]
 
 
 class SchedConfig(ctypes.Structure):
@@ -215,6 +218,23 @@ def _dt(t) -> str:
 
 
 _BF16 = ("bfloat16", "int16")  # bf16 values, or their raw 16-bit patterns
+
+
+def _rows(t, what: str, rows: int, heads: int, d: int) -> Tuple[Optional[int], int]:
+    """Address and token-row stride (elements) of a token-major [rows, heads, d] bf16 device
+    tensor whose heads are contiguous within a row; its rows may be further apart (a view
+    into a fused buffer).  None passes through with stride 0 (dense)."""
+    if t is None:
+        return None, 0
+    if not t.is_cuda:
+        raise ValueError(f"{what}: a device tensor is required")
+    if _dt(t) not in _BF16:
+        raise ValueError(f"{what}: dtype {t.dtype} is not one of {_BF16}")
+    if tuple(t.shape) != (rows, heads, d):
+        raise ValueError(f"{what}: shape {tuple(t.shape)}, expected {(rows, heads, d)}")
+    if rows and (t.stride(2) != 1 or (heads > 1 and t.stride(1) != d)):
+        raise ValueError(f"{what}: heads and channels must be contiguous within a token row")
+    return t.data_ptr(), (t.stride(0) if rows > 1 else heads * d)
 _F32 = ("float32",)
 
 
@@ -229,11 +249,20 @@ def _check(rc: int, what: str):
         raise HydraError(rc, what)
 
 
+def _set_rows(p: Problem, q, k, v):
+    """Checks q, k, v against the problem and records their token-row strides in it."""
+    qp, p.c.q_tok_stride = _rows(q, "q", p.nq, p.n_heads, 192)
+    kp, p.c.k_tok_stride = _rows(k, "k", p.nk, p.n_kv_heads, 192)
+    vp, p.c.v_tok_stride = _rows(v, "v", p.nk, p.n_kv_heads, 128)
+    return qp, kp, vp
+
+
 def attn_fwd(p: Problem, q, k, v, o_part, lse_part, workspace, o_bf16=None, stream=None):
-    """Partial O (fp32) and LSE of one ring step; optional bf16 copy of O."""
-    nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
-    _check(lib().hydra_attn_fwd(p.ref, _ptr(q, "q", _BF16, nqh * 192), _ptr(k, "k", _BF16, nkh * 192),
-                                _ptr(v, "v", _BF16, nkh * 128), _ptr(o_part, "o_part", _F32, nqh * 128),
+    """Partial O (fp32) and LSE of one ring step; optional bf16 copy of O.  q, k, v may be
+    views whose token rows are further apart than dense (e.g. slices of a fused buffer)."""
+    nqh = p.nq * p.n_heads
+    qp, kp, vp = _set_rows(p, q, k, v)
+    _check(lib().hydra_attn_fwd(p.ref, qp, kp, vp, _ptr(o_part, "o_part", _F32, nqh * 128),
                                 _ptr(lse_part, "lse_part", _F32, nqh), _ptr(o_bf16, "o_bf16", _BF16, nqh * 128),
                                 _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
                                 _stream(stream)), "hydra_attn_fwd")
@@ -241,10 +270,10 @@ def attn_fwd(p: Problem, q, k, v, o_part, lse_part, workspace, o_bf16=None, stre
 
 def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
              stream=None):
-    """dQ/dK/dV of one ring step, accumulated (+=) into fp32 buffers."""
+    """dQ/dK/dV of one ring step, accumulated (+=) into fp32 buffers (q, k, v as in attn_fwd)."""
     nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
-    _check(lib().hydra_attn_bwd(p.ref, _ptr(q, "q", _BF16, nqh * 192), _ptr(k, "k", _BF16, nkh * 192),
-                                _ptr(v, "v", _BF16, nkh * 128), _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
+    qp, kp, vp = _set_rows(p, q, k, v)
+    _check(lib().hydra_attn_bwd(p.ref, qp, kp, vp, _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
                                 _ptr(lse_final, "lse_final", _F32, nqh), _ptr(d_o, "d_o", _BF16, nqh * 128),
                                 _ptr(dq_acc, "dq_acc", _F32, nqh * 192), _ptr(dk_acc, "dk_acc", _F32, nkh * 192),
                                 _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _ptr(workspace, "workspace"),

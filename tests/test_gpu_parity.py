@@ -227,6 +227,9 @@ def test_binding_refuses_strided_mistyped_and_missized_tensors():
     o = torch.zeros((64, H, D_V), device="cuda")
     lse = torch.zeros((H, 64), device="cuda")
     with pytest.raises(ValueError, match="contiguous"):
+        hydra.attn_fwd(p, torch.zeros((64, D_QK, H), dtype=torch.bfloat16, device="cuda").transpose(1, 2), q, v,
+                       o, lse, ws)
+    with pytest.raises(ValueError, match="shape"):
         hydra.attn_fwd(p, q.transpose(0, 1), q, v, o, lse, ws)
     with pytest.raises(ValueError, match="dtype"):
         hydra.attn_fwd(p, q.float(), q, v, o, lse, ws)
@@ -235,6 +238,45 @@ def test_binding_refuses_strided_mistyped_and_missized_tensors():
     with pytest.raises(ValueError, match="dtype"):
         hydra.pack_heads(q, torch.empty((2, 64, 1, D_QK), device="cuda"), 2)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("layout,H,Hkv", [("ragged_3step", 3, 0), ("zigzag_2step", 8, 2)])
+def test_strided_qkv_views_match_dense(layout, H, Hkv):
+    """Q, K, V as views into fused per-token buffers (token rows further apart than dense,
+    heads contiguous): every output equals the dense run bit for bit."""
+    cu, q_segs, steps = MEDIUM[layout]
+    Hk = Hkv or H
+    q, kv, do = _gen(cu, H, q_segs, steps, dist="sharp", seed=4, bwd=True, Hkv=Hkv)
+    dense = _run_share(cu, H, q_segs, steps, q, kv, do, Hkv=Hkv)
+
+    def fused(parts):
+        """One buffer [rows, sum(widths) + 8] holding the parts side by side; the views."""
+        rows = parts[0].shape[0]
+        widths = [p.shape[1] * p.shape[2] for p in parts]
+        buf = torch.zeros((rows, sum(widths) + 8), dtype=torch.bfloat16, device="cuda")
+        views, c = [], 0
+        for p, w in zip(parts, widths):
+            buf[:, c:c + w] = dev_bf16(p).reshape(rows, w)
+            views.append(buf[:, c:c + w].view(rows, p.shape[1], p.shape[2]))
+            c += w
+        return buf, views
+
+    qbuf, (qv,) = fused([q])
+    kvbufs = [fused([k, v]) for k, v in kv]
+    kvv = [tuple(views) for _, views in kvbufs]
+    assert qv.stride(0) > H * D_QK and kvv[0][0].stride(0) > Hk * D_QK
+    sh = ring.make_share(cu, H, q_segs, steps, n_kv_heads=Hkv)
+    o, lse, o16 = ring.forward(sh, qv, kvv)
+    d_o = dev_bf16(do)
+    dq = torch.zeros((sh.nq, H, D_QK), device="cuda")
+    dkv = [(torch.zeros((k.shape[0], Hk, D_QK), device="cuda"), torch.zeros((k.shape[0], Hk, D_V), device="cuda"))
+           for k, _ in kv]
+    ring.backward(sh, qv, kvv, d_o, dq, dkv)
+    torch.cuda.synchronize()
+    assert np.array_equal(o.cpu().numpy(), dense["o"]) and np.array_equal(lse.cpu().numpy(), dense["lse"])
+    assert np.array_equal(dq.cpu().numpy(), dense["dq"])
+    for (a, b), (c, d) in zip(dkv, dense["dkv"]):
+        assert np.array_equal(a.cpu().numpy(), c) and np.array_equal(b.cpu().numpy(), d)
 
 
 def test_gradient_canaries_untouched():

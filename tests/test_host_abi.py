@@ -164,6 +164,22 @@ def test_binding_refuses_host_tensors():
         hydra.pack_heads(q, q, 2)
 
 
+def test_token_strides_checked_on_host():
+    """q/k/v token strides: 0 or at least dense, a multiple of 8, below 2^22."""
+    def ws(**strides):
+        p = _problem([0, 64], 2, [(0, 64)], [(0, 64)], n_kv_heads=1)
+        for name, val in strides.items():
+            setattr(p.c, name, val)
+        return hydra.workspace_size(p)
+    assert ws() > 0
+    assert ws(q_tok_stride=2 * 192 + 8, k_tok_stride=192 + 128, v_tok_stride=192 + 128 + 8) > 0
+    assert ws(q_tok_stride=2 * 192 - 8) == 0          # below dense
+    assert ws(k_tok_stride=191) == 0                  # below dense for one K/V head
+    assert ws(v_tok_stride=128 + 4) == 0              # rows not 16-byte aligned
+    assert ws(q_tok_stride=1 << 22) == 0              # too far apart
+    assert ws(v_tok_stride=-8) == 0
+
+
 def test_launch_size_limit_checked_on_host():
     """One 512-lane workgroup per (tile, head) and fewer than 2^32 lanes per dispatch:
     2^23 (query tile, head) pairs are refused, one fewer is planned."""

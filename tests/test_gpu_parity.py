@@ -180,6 +180,48 @@ def test_constant_v_gives_constant_and_single_key_rows():
         np.testing.assert_allclose(res["lse"][:, r], s_rr, atol=TOL_LSE)
 
 
+def test_thousands_of_tiny_documents():
+    """2500 documents of 1-4 tokens, one zero-length, in one segment: every tile straddles
+    many document starts.  Single-token documents see only themselves: O = V, dV = dO, and
+    dQ = dK = 0 up to rounding (dS = P (dP - D) with dP and D two fp32 evaluations of the
+    same 128-term dot product); everything against the oracle, forward and backward."""
+    rng = np.random.default_rng(8)
+    lens = rng.integers(1, 5, size=2500)
+    lens[7] = 0
+    cu = [0] + list(np.cumsum(lens))
+    segs = [(0, int(cu[-1]))]
+    H = 2
+    q, kv, do = _gen(cu, H, segs, [segs], dist="sharp", seed=8, bwd=True)
+    res = _run_share(cu, H, segs, [segs], q, kv, do)
+    ref = _oracle_share(cu, segs, [segs], q, kv, do)
+    _check_fwd(res, ref)
+    _check_bwd(res, ref)
+    ones = [int(cu[d]) for d in range(len(lens)) if lens[d] == 1]
+    np.testing.assert_allclose(res["o"][ones], f32(kv[0][1])[ones], atol=1e-6)
+    assert np.abs(res["dq"][ones]).max() <= 1e-5 * np.abs(res["dq"]).max()
+    assert np.abs(res["dkv"][0][0][ones]).max() <= 1e-5 * np.abs(res["dkv"][0][0]).max()
+    np.testing.assert_allclose(res["dkv"][0][1][ones], f32(do)[ones], atol=1e-6)
+
+
+def test_largest_head_count():
+    """4096 heads (the largest accepted): token rows of 786432 elements; two short documents,
+    a handful of heads checked against the oracle, forward and backward."""
+    cu, segs, H = [0, 40, 72], [(0, 72)], 4096
+    rng = np.random.default_rng(9)
+    draw = lambda d, sc: inputs.bf16_round_bits(rng.standard_normal((72, H, d), dtype=np.float32) * np.float32(sc))
+    q, kv, do = draw(D_QK, D_QK ** -0.5), [(draw(D_QK, D_QK ** -0.5), draw(D_V, D_V ** -0.5))], draw(D_V, 1.0)
+    res = _run_share(cu, H, segs, [segs], q, kv, do)
+    heads = [0, 1, 2047, 4095]
+    sub = lambda x: f32(x)[:, heads]
+    O, L = oracle.attn_fwd(sub(q), sub(kv[0][0]), sub(kv[0][1]), cu, segs, segs)
+    dq, dk, dv = oracle.attn_bwd(sub(q), sub(kv[0][0]), sub(kv[0][1]), O, L, sub(do), cu, segs, segs)
+    assert_o_close(res["o"][:, heads], O)
+    assert_lse_close(res["lse"][heads], L)
+    assert_grad_close(res["dq"][:, heads], dq, what="dQ")
+    assert_grad_close(res["dkv"][0][0][:, heads], dk, what="dK")
+    assert_grad_close(res["dkv"][0][1][:, heads], dv, what="dV")
+
+
 def test_empty_kv_chunk_and_fully_masked_step():
     cu = [0, 700]
     q_segs = [(300, 200)]

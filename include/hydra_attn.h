@@ -85,7 +85,8 @@ typedef struct {
 } hydra_problem_t;
 
 /* Size limits (HYDRA_ERR_INVALID beyond them): n_heads <= 4096; Nq, Nk <= 2^30 rows;
- * Nq * n_heads * 192 and Nk * n_heads * 192 below 2^40 elements; and, because every
+ * Nq * n_heads * 192, Nk * n_heads * 192, Nq * q_tok_stride and Nk * k_tok_stride below
+ * 2^40 elements; and, because every
  * attention launch holds one 512-lane workgroup per (tile, head) and a dispatch fewer than
  * 2^32 lanes, (sum over the query segments of ceil(len / 256)) * n_heads and (sum over the
  * K/V segments of ceil(len / 128)) * n_kv_heads below 2^23.

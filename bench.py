@@ -111,6 +111,9 @@ def main() -> int:
                     help="K/V heads (grouped-query attention); 0: one per query head (MLA)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this size first (counter calibration)")
+    ap.add_argument("--graph", action="store_true",
+                    help="plan once, record one step into a HIP graph and time its replays "
+                         "(per-kernel times then come from one eager step of the same calls)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
@@ -147,34 +150,48 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    sh = ring.make_share(w.cu_seqlens, H, w.q_segs, w.kv_steps, n_kv_heads=Hkv)
+    sh = ring.make_share(w.cu_seqlens, H, w.q_segs, w.kv_steps, n_kv_heads=Hkv, graph_ready=args.graph)
+    if args.graph:
+        ring.plan(sh)
     pairs_step = [hydra.visible_pairs(p) for p in sh.problems]
     dq = torch.empty((sh.nq, H, D_QK), dtype=torch.float32, device="cuda")
     dkv = [(torch.empty((k.shape[0], Hkv, D_QK), dtype=torch.float32, device="cuda"),
             torch.empty((k.shape[0], Hkv, D_V), dtype=torch.float32, device="cuda")) for k, _ in kv]
 
     def step():
-        dq.zero_()
+        dq.fill_(0.0)
         for a, b in dkv:
-            a.zero_()
-            b.zero_()
-        ring.forward(sh, q, kv)
-        ring.backward(sh, q, kv, d_o, dq, dkv)
+            a.fill_(0.0)
+            b.fill_(0.0)
+        ring.forward(sh, q, kv, planned=args.graph)
+        ring.backward(sh, q, kv, d_o, dq, dkv, planned=args.graph)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    hydra.profile_start()
+    run = step
+    if args.graph:
+        hydra.profile_start()  # per-kernel times from one eager step of the same calls
+        step()
+        prof = hydra.profile_stop()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        run = graph.replay
+        run()
+    else:
+        hydra.profile_start()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0.record()
     for _ in range(args.steps):
-        step()
+        run()
     ev1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    prof = hydra.profile_stop()
+    if not args.graph:
+        prof = hydra.profile_stop()
     ms_per_step = ev0.elapsed_time(ev1) / args.steps
 
     pairs = sum(pairs_step) * H
@@ -211,7 +228,8 @@ def main() -> int:
                    "n_heads": H, "n_kv_heads": Hkv, "d_qk": D_QK, "d_v": D_V, "ring_steps": len(w.kv_steps),
                    "q_segments": [list(s) for s in w.q_segs],
                    "visible_pairs_per_head": pairs_step, "counted_tflop_per_step": round(flop_step / 1e12, 3),
-                   "parallelism": PARALLELISM.get(w.name, "one rank")},
+                   "parallelism": PARALLELISM.get(w.name, "one rank"),
+                   "launch": "hip graph replay" if args.graph else "eager"},
         "pct_of_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "kernels": kernels,
         "roofline": roofline,

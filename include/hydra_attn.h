@@ -124,6 +124,24 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
                    float* dq_acc, float* dk_acc, float* dv_acc,
                    void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that record the calls into a HIP graph (stream capture), where the plan's
+ * host-to-device copy cannot be recorded: hydra_attn_plan uploads the complete work plan of
+ * `p` (both sides) into `workspace` once, outside the capture; the *_planned calls then take
+ * exactly the arguments of hydra_attn_fwd / hydra_attn_bwd, check them the same way on the
+ * host, and only launch kernels (no copy, no host-side wait), reading the plan from the
+ * workspace.  The workspace must hold the plan of this same problem (same cu_seqlens,
+ * chunks and head counts; strides may differ) and must not be reused for another problem
+ * while a recorded graph still uses it; one workspace per ring step.  The backward writes
+ * D and LSE*log2(e) into the workspace as before. */
+int hydra_attn_plan(const hydra_problem_t* p, void* workspace, size_t workspace_bytes, void* stream);
+int hydra_attn_fwd_planned(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                           float* o_part, float* lse_part, void* o_part_bf16,
+                           void* workspace, size_t workspace_bytes, void* stream);
+int hydra_attn_bwd_planned(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                           const void* o_final, const float* lse_final, const void* d_o,
+                           float* dq_acc, float* dk_acc, float* dv_acc,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
 /* Exact merge of two partials of the same rows (ring CP, Sec. 5.2.2):
  *   L = log(e^La + e^Lb),  O = e^(La-L) O_a + e^(Lb-L) O_b, in place into (o_acc, lse_acc).
  * (0, -inf) is the identity; two empty rows stay (0, -inf) with no NaN.

@@ -152,8 +152,14 @@ size_t hydra_workspace_size(const hydra_problem_t* p) {
   return ws_layout(pr).total;
 }
 
-int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, float* o_part,
-                   float* lse_part, void* o_bf16, void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Forward of one ring step; `upload` = false launches only (the plan is already in the
+// workspace, from hydra_attn_plan).
+int attn_fwd_impl(bool upload, const hydra_problem_t* p, const void* q, const void* k, const void* v, float* o_part,
+                  float* lse_part, void* o_bf16, void* workspace, size_t workspace_bytes, void* stream) {
   try {
     Problem pr;
     int rc = check_problem(p, &pr);
@@ -173,9 +179,11 @@ int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const
                         {{q, qb}, {k, kb}, {v, vb}}))
       return HYDRA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    std::vector<int32_t> qitems, kitems;
-    rc = upload_plan(pr, w, false, workspace, s, &qitems, &kitems);
-    if (rc != HYDRA_OK) return rc;
+    if (upload) {  // the forward needs only the query-stationary items
+      std::vector<int32_t> qitems, kitems;
+      rc = upload_plan(pr, w, false, workspace, s, &qitems, &kitems);
+      if (rc != HYDRA_OK) return rc;
+    }
     AttnArgs a = base_args(pr, w, workspace);
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);
@@ -190,9 +198,9 @@ int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const
   }
 }
 
-int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, const void* o_final,
-                   const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc, float* dv_acc,
-                   void* workspace, size_t workspace_bytes, void* stream) {
+int attn_bwd_impl(bool upload, const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                  const void* o_final, const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc,
+                  float* dv_acc, void* workspace, size_t workspace_bytes, void* stream) {
   try {
     Problem pr;
     int rc = check_problem(p, &pr);
@@ -214,9 +222,11 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
                          {d_o, qh * kDv * 2}}))
       return HYDRA_ERR_INVALID;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    std::vector<int32_t> qitems, kitems;
-    rc = upload_plan(pr, w, true, workspace, s, &qitems, &kitems);
-    if (rc != HYDRA_OK) return rc;
+    if (upload) {
+      std::vector<int32_t> qitems, kitems;
+      rc = upload_plan(pr, w, true, workspace, s, &qitems, &kitems);
+      if (rc != HYDRA_OK) return rc;
+    }
     AttnArgs a = base_args(pr, w, workspace);
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);
@@ -233,6 +243,49 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
   } catch (...) {
     return HYDRA_ERR_INVALID;
   }
+}
+
+}  // namespace
+
+extern "C" {
+
+int hydra_attn_plan(const hydra_problem_t* p, void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    Problem pr;
+    int rc = check_problem(p, &pr);
+    if (rc != HYDRA_OK) return rc;
+    const WsLayout w = ws_layout(pr);
+    if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
+    std::vector<int32_t> qitems, kitems;
+    return upload_plan(pr, w, true, workspace, static_cast<hipStream_t>(stream), &qitems, &kitems);
+  } catch (...) {
+    return HYDRA_ERR_INVALID;
+  }
+}
+
+int hydra_attn_fwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, float* o_part,
+                   float* lse_part, void* o_bf16, void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_fwd_impl(true, p, q, k, v, o_part, lse_part, o_bf16, workspace, workspace_bytes, stream);
+}
+
+int hydra_attn_fwd_planned(const hydra_problem_t* p, const void* q, const void* k, const void* v, float* o_part,
+                           float* lse_part, void* o_bf16, void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_fwd_impl(false, p, q, k, v, o_part, lse_part, o_bf16, workspace, workspace_bytes, stream);
+}
+
+int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, const void* o_final,
+                   const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc, float* dv_acc,
+                   void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_bwd_impl(true, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
+                       workspace_bytes, stream);
+}
+
+int hydra_attn_bwd_planned(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                           const void* o_final, const float* lse_final, const void* d_o, float* dq_acc,
+                           float* dk_acc, float* dv_acc, void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_bwd_impl(false, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
+                       workspace_bytes, stream);
 }
 
 int hydra_lse_merge(int64_t n_rows, int32_t n_heads, int32_t d_v, float* o_acc, float* lse_acc,

@@ -95,6 +95,12 @@ def lib() -> ctypes.CDLL:
         L.hydra_attn_fwd.restype = ctypes.c_int
         L.hydra_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.hydra_attn_bwd.restype = ctypes.c_int
+        L.hydra_attn_plan.argtypes = [P, vp, ctypes.c_size_t, vp]
+        L.hydra_attn_plan.restype = ctypes.c_int
+        L.hydra_attn_fwd_planned.argtypes = L.hydra_attn_fwd.argtypes
+        L.hydra_attn_fwd_planned.restype = ctypes.c_int
+        L.hydra_attn_bwd_planned.argtypes = L.hydra_attn_bwd.argtypes
+        L.hydra_attn_bwd_planned.restype = ctypes.c_int
         L.hydra_lse_merge.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, vp, vp, vp]
         L.hydra_lse_merge.restype = ctypes.c_int
         L.hydra_strerror.argtypes = [ctypes.c_int]
@@ -257,23 +263,35 @@ def _set_rows(p: Problem, q, k, v):
     return qp, kp, vp
 
 
-def attn_fwd(p: Problem, q, k, v, o_part, lse_part, workspace, o_bf16=None, stream=None):
+def attn_plan(p: Problem, workspace, stream=None):
+    """Uploads the complete work plan of p into workspace (outside any graph capture), for
+    the planned calls below."""
+    _check(lib().hydra_attn_plan(p.ref, _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)), "hydra_attn_plan")
+
+
+def attn_fwd(p: Problem, q, k, v, o_part, lse_part, workspace, o_bf16=None, stream=None, planned=False):
     """Partial O (fp32) and LSE of one ring step; optional bf16 copy of O.  q, k, v may be
-    views whose token rows are further apart than dense (e.g. slices of a fused buffer)."""
+    views whose token rows are further apart than dense (e.g. slices of a fused buffer).
+    planned: the workspace already holds p's plan (attn_plan); only kernels are launched,
+    so the call can be recorded into a graph."""
     nqh = p.nq * p.n_heads
     qp, kp, vp = _set_rows(p, q, k, v)
-    _check(lib().hydra_attn_fwd(p.ref, qp, kp, vp, _ptr(o_part, "o_part", _F32, nqh * 128),
+    fn = lib().hydra_attn_fwd_planned if planned else lib().hydra_attn_fwd
+    _check(fn(p.ref, qp, kp, vp, _ptr(o_part, "o_part", _F32, nqh * 128),
                                 _ptr(lse_part, "lse_part", _F32, nqh), _ptr(o_bf16, "o_bf16", _BF16, nqh * 128),
                                 _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
                                 _stream(stream)), "hydra_attn_fwd")
 
 
 def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
-             stream=None):
-    """dQ/dK/dV of one ring step, accumulated (+=) into fp32 buffers (q, k, v as in attn_fwd)."""
+             stream=None, planned=False):
+    """dQ/dK/dV of one ring step, accumulated (+=) into fp32 buffers (q, k, v and planned as
+    in attn_fwd)."""
     nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
     qp, kp, vp = _set_rows(p, q, k, v)
-    _check(lib().hydra_attn_bwd(p.ref, qp, kp, vp, _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
+    fn = lib().hydra_attn_bwd_planned if planned else lib().hydra_attn_bwd
+    _check(fn(p.ref, qp, kp, vp, _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
                                 _ptr(lse_final, "lse_final", _F32, nqh), _ptr(d_o, "d_o", _BF16, nqh * 128),
                                 _ptr(dq_acc, "dq_acc", _F32, nqh * 192), _ptr(dk_acc, "dk_acc", _F32, nkh * 192),
                                 _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _ptr(workspace, "workspace"),

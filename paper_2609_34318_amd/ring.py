@@ -22,7 +22,8 @@ D_QK, D_V = 192, 128
 class Share:
     """Problems and device buffers for one rank's share."""
     problems: List[hydra.Problem]
-    workspace: torch.Tensor
+    workspace: torch.Tensor          # shared by the steps when each call uploads its plan
+    step_workspaces: Optional[List[torch.Tensor]]  # one per step, for planned (graph) calls
     o_acc: torch.Tensor
     lse_acc: torch.Tensor
     o_tmp: Optional[torch.Tensor]
@@ -39,8 +40,10 @@ class Share:
 
 
 def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cuda",
-               softmax_scale: float = 0.0, n_kv_heads: int = 0) -> Share:
-    """Plans every ring step of one rank; n_kv_heads (0: n_heads) < n_heads for grouped K/V."""
+               softmax_scale: float = 0.0, n_kv_heads: int = 0, graph_ready: bool = False) -> Share:
+    """Plans every ring step of one rank; n_kv_heads (0: n_heads) < n_heads for grouped K/V.
+    graph_ready: one workspace per step, for plan() and the planned calls that a graph can
+    record."""
     probs = [hydra.Problem(cu_seqlens, n_heads, q_segs, s, softmax_scale, n_kv_heads=n_kv_heads) for s in kv_steps]
     ws = max(hydra.workspace_size(p) for p in probs)
     if ws == 0:
@@ -51,6 +54,8 @@ def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cud
     return Share(
         problems=probs,
         workspace=torch.empty(ws, dtype=torch.uint8, device=device),
+        step_workspaces=[torch.empty(hydra.workspace_size(p), dtype=torch.uint8, device=device) for p in probs]
+        if graph_ready else None,
         o_acc=torch.empty((nq, n_heads, D_V), **f32),
         lse_acc=torch.empty((n_heads, nq), **f32),
         o_tmp=torch.empty((nq, n_heads, D_V), **f32) if multi else None,
@@ -59,19 +64,35 @@ def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cud
     )
 
 
-def forward(sh: Share, q: torch.Tensor, kv: Sequence[Tuple[torch.Tensor, torch.Tensor]]):
+def plan(sh: Share, stream=None):
+    """Uploads every step's plan into its own workspace (a graph_ready share), outside any
+    capture; afterwards forward/backward(planned=True) only launch kernels."""
+    if sh.step_workspaces is None:
+        raise ValueError("plan() needs a share made with graph_ready=True")
+    for p, ws in zip(sh.problems, sh.step_workspaces):
+        hydra.attn_plan(p, ws, stream)
+
+
+def _ws(sh: Share, i: int, planned: bool):
+    return sh.step_workspaces[i] if planned else sh.workspace
+
+
+def forward(sh: Share, q: torch.Tensor, kv: Sequence[Tuple[torch.Tensor, torch.Tensor]], planned: bool = False):
     """Runs every ring step and the merges; returns (O fp32, LSE, O bf16)."""
     n = len(sh.problems)
     for i, (p, (k, v)) in enumerate(zip(sh.problems, kv)):
+        ws = _ws(sh, i, planned)
         if i == 0:
-            hydra.attn_fwd(p, q, k, v, sh.o_acc, sh.lse_acc, sh.workspace, o_bf16=sh.o_bf16 if n == 1 else None)
+            hydra.attn_fwd(p, q, k, v, sh.o_acc, sh.lse_acc, ws, o_bf16=sh.o_bf16 if n == 1 else None,
+                           planned=planned)
         else:
-            hydra.attn_fwd(p, q, k, v, sh.o_tmp, sh.lse_tmp, sh.workspace)
+            hydra.attn_fwd(p, q, k, v, sh.o_tmp, sh.lse_tmp, ws, planned=planned)
             hydra.lse_merge(sh.o_acc, sh.lse_acc, sh.o_tmp, sh.lse_tmp, o_bf16=sh.o_bf16 if i == n - 1 else None)
     return sh.o_acc, sh.lse_acc, sh.o_bf16
 
 
-def backward(sh: Share, q, kv, d_o, dq: torch.Tensor, dkv: Sequence[Tuple[torch.Tensor, torch.Tensor]]):
+def backward(sh: Share, q, kv, d_o, dq: torch.Tensor, dkv: Sequence[Tuple[torch.Tensor, torch.Tensor]],
+             planned: bool = False):
     """Accumulates dQ (over steps) and each step's dK/dV; buffers are += targets."""
-    for p, (k, v), (dk, dv) in zip(sh.problems, kv, dkv):
-        hydra.attn_bwd(p, q, k, v, sh.o_bf16, sh.lse_acc, d_o, dq, dk, dv, sh.workspace)
+    for i, (p, (k, v), (dk, dv)) in enumerate(zip(sh.problems, kv, dkv)):
+        hydra.attn_bwd(p, q, k, v, sh.o_bf16, sh.lse_acc, d_o, dq, dk, dv, _ws(sh, i, planned), planned=planned)

@@ -25,7 +25,8 @@ def test_library_exports_every_declared_function():
     for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
         text = open(os.path.join(ROOT, "include", h)).read()
         names |= set(re.findall(r"\b(hydra_[a-z0-9_]+)\s*\(", text))
-    assert {"hydra_attn_fwd", "hydra_attn_bwd", "hydra_lse_merge", "hydra_workspace_size",
+    assert {"hydra_attn_fwd", "hydra_attn_bwd", "hydra_lse_merge", "hydra_workspace_size", "hydra_attn_plan",
+            "hydra_attn_fwd_planned", "hydra_attn_bwd_planned",
             "hydra_pack_heads", "hydra_unpack_heads", "hydra_zigzag_gather", "hydra_zigzag_scatter",
             "hydra_unpack_heads_gated", "hydra_pack_heads_gated_bwd", "hydra_schedule"} <= names
     L = hydra.lib()
@@ -102,6 +103,9 @@ def test_invalid_problems_rejected_on_host(case):
     L = hydra.lib()
     assert L.hydra_attn_fwd(p.ref, None, None, None, None, None, None, None, 0, None) == -1
     assert L.hydra_attn_bwd(p.ref, *([None] * 10), 0, None) == -1
+    assert L.hydra_attn_plan(p.ref, None, 0, None) == -1
+    assert L.hydra_attn_fwd_planned(p.ref, None, None, None, None, None, None, None, 0, None) == -1
+    assert L.hydra_attn_bwd_planned(p.ref, *([None] * 10), 0, None) == -1
 
 
 def test_unsupported_dims_and_bad_pointers():
@@ -116,6 +120,9 @@ def test_unsupported_dims_and_bad_pointers():
     # workspace too small / missing
     assert L.hydra_attn_fwd(p.ref, 16, 16, 16, 16, 16, None, 16, ws - 1, None) == -4
     assert L.hydra_attn_fwd(p.ref, 16, 16, 16, 16, 16, None, None, ws, None) == -4
+    assert L.hydra_attn_plan(p.ref, 16, ws - 1, None) == -4
+    assert L.hydra_attn_plan(p.ref, 8, ws, None) == -3
+    assert L.hydra_attn_fwd_planned(p.ref, 8, 16, 16, 16, 16, None, 16, ws, None) == -3
     # merge argument checks
     assert L.hydra_lse_merge(10, 2, 64, 16, 16, 16, 16, None, None) == -2
     assert L.hydra_lse_merge(-1, 2, 128, 16, 16, 16, 16, None, None) == -1

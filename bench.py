@@ -17,6 +17,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -35,10 +36,22 @@ PEAK_BF16_TFLOPS = 2516.6                        # 256 CU x 4096 FLOP/clk x 2.4 
 KERNEL_SOURCES = {"attn_fwd": "attn_fwd.hip", "bwd_dkdv": "attn_bwd.hip", "bwd_dq": "attn_bwd.hip"}
 
 
+def _code(path: str) -> bytes:
+    """A source file without comments and with whitespace collapsed: what the compiler sees."""
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split()).encode()
+
+
 def _source_sha(kernel: str) -> str:
-    path = os.path.join(ROOT, "paper_2609_34318_amd", "csrc", KERNEL_SOURCES[kernel])
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the code a kernel is built from (its source and the shared header)."""
+    csrc = os.path.join(ROOT, "paper_2609_34318_amd", "csrc")
+    h = hashlib.sha256()
+    for name in (KERNEL_SOURCES[kernel], "kernels.h"):
+        h.update(_code(os.path.join(csrc, name)))
+    return h.hexdigest()[:16]
 
 
 def _traffic(kernel: str, workload: str):

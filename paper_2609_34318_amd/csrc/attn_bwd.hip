@@ -212,8 +212,8 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
 constexpr int KV_BQ = 96;                                        // query rows per tile
 constexpr int KV_NSB = KV_BQ / 32;                               // 32-row sub-blocks per tile
 constexpr int KV_VEC = 128;                                      // LDS slots per vector (LSE2, D)
-constexpr int KV_QBYTES = KV_BQ * DQK * 2;                       // 24 KB
-constexpr int KV_OBYTES = KV_BQ * DV * 2;                        // 16 KB
+constexpr int KV_QBYTES = KV_BQ * DQK * 2;                       // 36 KB
+constexpr int KV_OBYTES = KV_BQ * DV * 2;                        // 24 KB
 constexpr int KV_STAGE = KV_QBYTES + KV_OBYTES + 2 * KV_VEC * 4;  // + LSE2 and D
 constexpr int KV_NSTAGE = 2;  // measured faster than three stages
 constexpr int KV_PBYTES = 4 * KV_NSB * 2048;                     // P: 4 pairs x sub-blocks x 32x32 bf16

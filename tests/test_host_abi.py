@@ -200,6 +200,17 @@ def test_launch_size_limit_checked_on_host():
     assert hydra.workspace_size(kv_big) == 0
 
 
+def test_ring_plan_needs_per_step_workspaces():
+    """Planned (graph-recordable) calls need one workspace per ring step."""
+    from paper_2609_34318_amd import ring
+    cu, q, steps = [0, 512], [(0, 256)], [[(0, 128)], [(128, 128)]]
+    sh = ring.make_share(cu, 2, q, steps, device="cpu")
+    with pytest.raises(ValueError, match="graph_ready"):
+        ring.plan(sh)
+    sh = ring.make_share(cu, 2, q, steps, device="cpu", graph_ready=True)
+    assert [w.numel() for w in sh.step_workspaces] == [hydra.workspace_size(p) for p in sh.problems]
+
+
 def test_zero_rows_is_noop():
     L = hydra.lib()
     p = _problem([0, 64], 2, [], [(0, 64)])

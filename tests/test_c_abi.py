@@ -99,3 +99,18 @@ def test_c_program_matches_the_binding(tmp_path, lib_path):
     assert got["tiles"] == "%d %d" % hydra.tile_rows()
     assert got["status"] == hydra.lib().hydra_strerror(-4).decode()
     assert int(got["fwd_null"]) == -1 and int(got["unsupported"]) == -2 and int(got["bad_stride"]) == 0
+
+
+@pytest.mark.gpu
+def test_c_program_runs_the_forward_without_torch(tmp_path, lib_path):
+    """tests/c_abi_forward.c: hipMalloc'd buffers, hydra_attn_fwd from C, the uniform-softmax
+    closed form checked in the program itself."""
+    exe = tmp_path / "c_abi_forward"
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                        f"-I{INC}", os.path.join(ROOT, "tests", "c_abi_forward.c"), f"-L{PKG}", "-lhydra_attn",
+                        "-L/opt/rocm/lib", "-lamdhip64", "-lm", f"-Wl,-rpath,{PKG}", "-Wl,-rpath,/opt/rocm/lib",
+                        "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    print(r.stdout.strip())
+    assert r.returncode == 0, r.stdout + r.stderr

@@ -21,7 +21,7 @@
  *     pruned; a min-heap drives backfill; the pool maximum for the balance test is kept
  *     incrementally.  O(N log G) per batch; the placement is identical to linear scans.
  *
- * Readings where the paper is silent (the reference implementation makes the same ones):
+ * Readings where the paper is silent:
  *   1. A new group needs a free k-aligned block of ranks; the lowest one is taken.  G must
  *      be a multiple of C*.
  *   2. Equal lengths keep their input order; among equally small, equally loaded feasible

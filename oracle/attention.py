@@ -252,28 +252,34 @@ def uniform_bwd_k0(q, v, o, do, n_total, cu_seqlens, q_segs, kv_segs, key_rows,
     row sees over the whole ring.  For a key j of this step's chunk, with the sums
     over the queries i that see it:
         dV_j = sum_i dO_i / n_i,   dK_j = tau * sum_i (<dO_i, v_j> - D_i) q_i / n_i.
-    (dQ is exactly zero since K = 0.)  Returns arrays [len(key_rows), H_sel, d].
+    (dQ is exactly zero since K = 0.)  With grouped K/V heads (v has Hkv < H heads) the
+    gradient of K/V head g sums these over its query heads g*grp .. g*grp + grp-1,
+    grp = H / Hkv (Sec. 3.5: one K/V head serves a group of query heads).  ``heads``
+    selects K/V heads.  Returns arrays [len(key_rows), len(heads), d].
     """
     Q, V, O, dO = _f64(q), _f64(v), _f64(o), _f64(do)
     nq, H, dqk = Q.shape
+    Hkv = V.shape[1]
+    grp = _group(H, Hkv)
     tau = default_scale(dqk) if scale is None else float(scale)
     qpos, kpos = row_positions(q_segs), row_positions(kv_segs)
     cu = np.asarray(cu_seqlens, dtype=np.int64)
     qdoc = doc_of(cu, qpos)
     kdoc = doc_of(cu, kpos)
     key_rows = np.asarray(key_rows)
-    hs = list(range(H) if heads is None else heads)
+    hs = list(range(Hkv) if heads is None else heads)
     dK = np.zeros((len(key_rows), len(hs), dqk))
     dV = np.zeros((len(key_rows), len(hs), V.shape[2]))
     inv_n = np.where(n_total > 0, 1.0 / np.maximum(n_total, 1), 0.0)
-    for hi, h in enumerate(hs):
-        D = np.einsum("nc,nc->n", dO[:, h, :], O[:, h, :])
-        for r, j in enumerate(key_rows):
-            sees = (qdoc == kdoc[j]) & (qpos >= kpos[j])
-            w = inv_n[sees]
-            dV[r, hi] = (w[:, None] * dO[sees, h, :]).sum(axis=0)
-            coef = w * (dO[sees, h, :] @ V[j, h, :] - D[sees])
-            dK[r, hi] = tau * (coef[:, None] * Q[sees, h, :]).sum(axis=0)
+    for hi, g in enumerate(hs):
+        for h in range(g * grp, (g + 1) * grp):
+            D = np.einsum("nc,nc->n", dO[:, h, :], O[:, h, :])
+            for r, j in enumerate(key_rows):
+                sees = (qdoc == kdoc[j]) & (qpos >= kpos[j])
+                w = inv_n[sees]
+                dV[r, hi] += (w[:, None] * dO[sees, h, :]).sum(axis=0)
+                coef = w * (dO[sees, h, :] @ V[j, g, :] - D[sees])
+                dK[r, hi] += tau * (coef[:, None] * Q[sees, h, :]).sum(axis=0)
     return dK, dV
 
 

@@ -368,6 +368,36 @@ def test_uniform_bwd_k0_matches_general_oracle():
     np.testing.assert_allclose(uv, dv[keys], atol=1e-12)
 
 
+def test_uniform_bwd_k0_grouped_heads_matches_general_oracle():
+    """Grouped K/V heads (8 query heads, 2 K/V heads): the closed form sums each K/V
+    head's gradient over its four query heads and indexes V by the group, as the general
+    oracle (pinned against SDPA on repeated heads) does."""
+    cu = [0, 70, 190]
+    full = [(0, 190)]
+    H, Hkv = 8, 2
+    q, _, _, g = _tensors(cu, full, full, H, dist="sharp", do=True)
+    _, _, v, _ = _tensors(cu, full, full, Hkv, dist="sharp")
+    k = np.zeros((190, Hkv, D_QK))
+    O, L = oracle.attn_fwd(q, k, v, cu, full, full)
+    dq, dk, dv = oracle.attn_bwd(q, k, v, O, L, g, cu, full, full)
+    np.testing.assert_array_equal(dq, 0.0)
+    Uo, UL, n = oracle.uniform_fwd(v, cu, full, full, n_q_heads=H)
+    np.testing.assert_allclose(Uo, O, atol=1e-12)
+    keys = np.array([0, 1, 69, 70, 71, 150, 189])
+    uk, uv = oracle.uniform_bwd_k0(q, v, Uo, g, n, cu, full, full, key_rows=keys)
+    assert uk.shape == (len(keys), Hkv, D_QK) and uv.shape == (len(keys), Hkv, D_V)
+    np.testing.assert_allclose(uk, dk[keys], atol=1e-12)
+    np.testing.assert_allclose(uv, dv[keys], atol=1e-12)
+    uk1, uv1 = oracle.uniform_bwd_k0(q, v, Uo, g, n, cu, full, full, key_rows=keys, heads=[1])
+    np.testing.assert_allclose(uk1[:, 0], dk[keys, 1], atol=1e-12)
+    np.testing.assert_allclose(uv1[:, 0], dv[keys, 1], atol=1e-12)
+    # a grouping that does not divide is refused rather than indexed past the end
+    with pytest.raises(ValueError, match="divide"):
+        oracle.uniform_bwd_k0(q[:, :7], v, Uo[:, :7], g[:, :7], n, cu, full, full, key_rows=keys)
+    with pytest.raises(ValueError, match="divide"):
+        oracle.uniform_bwd_k0(q, np.concatenate([v, v[:, :1]], axis=1), Uo, g, n, cu, full, full, key_rows=keys)
+
+
 # ------------------------------------------------------------ input recipe
 
 def test_packed_doc_list_reproduces_from_sampler():

@@ -124,6 +124,32 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
                    float* dq_acc, float* dk_acc, float* dv_acc,
                    void* workspace, size_t workspace_bytes, void* stream);
 
+/* Backward of one ring step without the dQ kernel's recomputation of S and dP (Sec. 3.5:
+ * the rank's cost is its S^2 h / P attention work, so work done twice is what to cut): the
+ * key-stationary kernel also stores dS (bf16, 2 bytes per visible (query, key) pair and
+ * query head) into ds_buf, and a query-stationary kernel reads it back for
+ * dQ += scale dS K.  Same arguments, results and checks as hydra_attn_bwd, plus
+ *   ds_buf   device scratch, 16-byte aligned, written and read by this call only (its
+ *            contents are meaningless afterwards); must not overlap any other argument
+ *   ds_bytes its size.  The heads are processed in passes of the largest number of K/V
+ *            heads whose query heads' dS fits: hydra_bwd_ds_bytes(p, g) bytes for g K/V
+ *            heads per pass (one pass holds all heads when ds_bytes >= hydra_bwd_ds_bytes(
+ *            p, n_kv_heads)).
+ * The path applies when every segment of both chunks starts at, and has a length that is, a
+ * multiple of 32 positions.  Otherwise, or when ds_bytes is below one K/V head's need, or
+ * ds_buf is NULL, the call computes exactly what hydra_attn_bwd computes, the same way.  The
+ * results are hydra_attn_bwd's up to rounding: dK and dV bit for bit, dQ from the dS that the
+ * dK/dV products use (formed from the bf16-rounded P) instead of a recomputed one. */
+int hydra_attn_bwd_ds(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                      const void* o_final, const float* lse_final, const void* d_o,
+                      float* dq_acc, float* dk_acc, float* dv_acc, void* ds_buf, size_t ds_bytes,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of ds_buf that hydra_attn_bwd_ds needs to process `kv_heads_per_pass` K/V heads (and
+ * their query heads) per pass; 0 when `p` is invalid or the stored-dS path does not apply
+ * (host only). */
+size_t hydra_bwd_ds_bytes(const hydra_problem_t* p, int32_t kv_heads_per_pass);
+
 /* For callers that record the calls into a HIP graph (stream capture), where the plan's
  * host-to-device copy cannot be recorded: hydra_attn_plan uploads the complete work plan of
  * `p` (both sides) into `workspace` once, outside the capture; the *_planned calls then take
@@ -132,7 +158,12 @@ int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const
  * workspace.  The workspace must hold the plan of this same problem (same cu_seqlens,
  * chunks and head counts; strides may differ) and must not be reused for another problem
  * while a recorded graph still uses it; one workspace per ring step.  The backward writes
- * D and LSE*log2(e) into the workspace as before. */
+ * D and LSE*log2(e) into the workspace as before.  The library remembers, per workspace
+ * address, which problem its last upload was for (hydra_attn_plan, or the upload inside
+ * hydra_attn_fwd / hydra_attn_bwd, where the forward's holds only the query-side items):
+ * a planned call on a workspace whose recorded plan is another problem's, or lacks the
+ * key-side items the backward needs, returns HYDRA_ERR_WORKSPACE before any HIP call.  A
+ * workspace freed and reallocated at the same address must be planned again. */
 int hydra_attn_plan(const hydra_problem_t* p, void* workspace, size_t workspace_bytes, void* stream);
 int hydra_attn_fwd_planned(const hydra_problem_t* p, const void* q, const void* k, const void* v,
                            float* o_part, float* lse_part, void* o_part_bf16,

@@ -16,7 +16,7 @@
 
 namespace hydra {
 hipError_t launch_attn_fwd(const AttnArgs& a, uint16_t* o_bf16, hipStream_t stream);
-hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems,
+hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems, int kv_heads_per_pass,
                            hipStream_t stream);
 hipError_t launch_lse_merge(int64_t n_rows, int H, float* o_acc, float* lse_acc, const float* o_part,
                             const float* lse_part, uint16_t* o_bf16, hipStream_t stream);
@@ -116,10 +116,57 @@ int upload_plan(const Problem& pr, const WsLayout& w, bool with_kv_items, void* 
   std::vector<char> img(bytes, 0);
   std::memcpy(img.data() + w.cu_off, pr.cu.data(), pr.cu.size() * sizeof(int32_t));
   std::memcpy(img.data() + w.qitems_off, qitems->data(), qitems->size() * sizeof(int32_t));
-  if (with_kv_items) std::memcpy(img.data() + w.kitems_off, kitems->data(), kitems->size() * sizeof(int32_t));
+  if (with_kv_items) {
+    std::memcpy(img.data() + w.kitems_off, kitems->data(), kitems->size() * sizeof(int32_t));
+    std::vector<int32_t> kbase, kmap32;
+    ds_tables(pr, *kitems, &kbase, &kmap32);
+    std::memcpy(img.data() + w.kbase_off, kbase.data(), kbase.size() * sizeof(int32_t));
+    std::memcpy(img.data() + w.kmap_off, kmap32.data(), kmap32.size() * sizeof(int32_t));
+  }
   // Pageable source: the runtime has consumed `img` when the call returns.
   if (hipMemcpyAsync(ws, img.data(), bytes, hipMemcpyHostToDevice, stream) != hipSuccess) return HYDRA_ERR_HIP;
   return HYDRA_OK;
+}
+
+// Which problem's plan each workspace holds, as far as this library uploaded it: the
+// planned calls launch on the plan in the workspace, so they refuse a workspace whose
+// plan was made for another problem (its row ranges would not fit the buffers) or that
+// holds only the forward's query-side items.  Keyed by the workspace address; every
+// upload through this library replaces the entry.
+struct PlanRecord {
+  std::vector<int64_t> key;  // what the plan depends on: heads, documents, both chunks
+  bool has_kitems = false;
+};
+std::mutex g_plans_mu;
+std::map<const void*, PlanRecord> g_plans;
+
+std::vector<int64_t> plan_key(const Problem& pr) {
+  std::vector<int64_t> k = {pr.H, pr.Hkv, int64_t(pr.cu.size())};
+  k.insert(k.end(), pr.cu.begin(), pr.cu.end());
+  for (const hydra_chunk_t* c : {&pr.q, &pr.kv}) {
+    k.push_back(c->n_segs);
+    for (int s = 0; s < c->n_segs; ++s) {
+      k.push_back(c->start[s]);
+      k.push_back(c->len[s]);
+    }
+  }
+  return k;
+}
+
+void record_plan(const void* ws, const Problem& pr, bool has_kitems) {
+  std::lock_guard<std::mutex> lock(g_plans_mu);
+  PlanRecord& r = g_plans[ws];
+  r.key = plan_key(pr);
+  r.has_kitems = has_kitems;
+}
+
+// True if `ws` holds pr's plan, with the key-side items when `need_kitems`.
+bool plan_matches(const void* ws, const Problem& pr, bool need_kitems) {
+  std::lock_guard<std::mutex> lock(g_plans_mu);
+  auto it = g_plans.find(ws);
+  if (it == g_plans.end()) return false;
+  if (need_kitems && !it->second.has_kitems) return false;
+  return it->second.key == plan_key(pr);
 }
 
 AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
@@ -129,10 +176,17 @@ AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
   a.items = reinterpret_cast<const int*>(base + w.qitems_off);
   a.Dvec = reinterpret_cast<float*>(base + w.d_off);
   a.lse2 = reinterpret_cast<float*>(base + w.lse2_off);
+  a.kitems = reinterpret_cast<const int*>(base + w.kitems_off);
+  a.kbase = reinterpret_cast<const int*>(base + w.kbase_off);
+  a.kmap32 = reinterpret_cast<const int*>(base + w.kmap_off);
   a.n_docs = int(pr.cu.size()) - 1;
   a.H = pr.H;
   a.Hkv = pr.Hkv;
   a.grp = pr.H / pr.Hkv;
+  a.kv_head0 = 0;
+  a.kv_heads = pr.Hkv;
+  a.q_head0 = 0;
+  a.q_heads = pr.H;
   a.nq = int(pr.nq);
   a.nk = int(pr.nk);
   a.q_s = pr.q_s;
@@ -183,6 +237,9 @@ int attn_fwd_impl(bool upload, const hydra_problem_t* p, const void* q, const vo
       std::vector<int32_t> qitems, kitems;
       rc = upload_plan(pr, w, false, workspace, s, &qitems, &kitems);
       if (rc != HYDRA_OK) return rc;
+      record_plan(workspace, pr, false);
+    } else if (!plan_matches(workspace, pr, false)) {
+      return HYDRA_ERR_WORKSPACE;
     }
     AttnArgs a = base_args(pr, w, workspace);
     a.q = static_cast<const uint16_t*>(q);
@@ -198,9 +255,18 @@ int attn_fwd_impl(bool upload, const hydra_problem_t* p, const void* q, const vo
   }
 }
 
+// Bytes of stored dS per query head on the stored-dS path (0 when the path does not apply).
+uint64_t ds_bytes_per_head(const Problem& pr) {
+  if (!ds_path_applies(pr)) return 0;
+  std::vector<int32_t> kitems, kbase, kmap32;
+  plan_items(pr, 1, &kitems);
+  return uint64_t(ds_tables(pr, kitems, &kbase, &kmap32)) * DS_TILE_BYTES;
+}
+
 int attn_bwd_impl(bool upload, const hydra_problem_t* p, const void* q, const void* k, const void* v,
                   const void* o_final, const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc,
-                  float* dv_acc, void* workspace, size_t workspace_bytes, void* stream) {
+                  float* dv_acc, void* ds_buf, size_t ds_bytes, void* workspace, size_t workspace_bytes,
+                  void* stream) {
   try {
     Problem pr;
     int rc = check_problem(p, &pr);
@@ -213,11 +279,21 @@ int attn_bwd_impl(bool upload, const hydra_problem_t* p, const void* q, const vo
     const WsLayout w = ws_layout(pr);
     if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
+    // stored-dS path: K/V heads per pass such that their query heads' dS fits ds_buf
+    int kv_per_pass = 0;
+    uint64_t ds_head = 0;
+    if (ds_buf) {
+      if (!aligned16(ds_buf)) return HYDRA_ERR_ALIGN;
+      ds_head = ds_bytes_per_head(pr);
+      const uint64_t per_kv = ds_head * uint64_t(pr.H / pr.Hkv);
+      if (per_kv > 0) kv_per_pass = int(std::min<uint64_t>(uint64_t(pr.Hkv), uint64_t(ds_bytes) / per_kv));
+    }
+    const uint64_t ds_used = uint64_t(kv_per_pass) * (pr.H / pr.Hkv) * ds_head;
     const uint64_t qh = uint64_t(pr.nq) * pr.H, kh = uint64_t(pr.nk) * pr.Hkv;
     const uint64_t qb = rows_bytes(pr.nq, pr.q_s, pr.H * kDqk), kb = rows_bytes(pr.nk, pr.k_s, pr.Hkv * kDqk),
                    vb = rows_bytes(pr.nk, pr.v_s, pr.Hkv * kDv);
     if (outputs_overlap({{dq_acc, qh * kDqk * 4}, {dk_acc, kh * kDqk * 4}, {dv_acc, kh * kDv * 4},
-                         {workspace, w.total}},
+                         {workspace, w.total}, {kv_per_pass ? ds_buf : nullptr, ds_used}},
                         {{q, qb}, {k, kb}, {v, vb}, {o_final, qh * kDv * 2}, {lse_final, qh * 4},
                          {d_o, qh * kDv * 2}}))
       return HYDRA_ERR_INVALID;
@@ -226,6 +302,9 @@ int attn_bwd_impl(bool upload, const hydra_problem_t* p, const void* q, const vo
       std::vector<int32_t> qitems, kitems;
       rc = upload_plan(pr, w, true, workspace, s, &qitems, &kitems);
       if (rc != HYDRA_OK) return rc;
+      record_plan(workspace, pr, true);
+    } else if (!plan_matches(workspace, pr, true)) {
+      return HYDRA_ERR_WORKSPACE;
     }
     AttnArgs a = base_args(pr, w, workspace);
     a.q = static_cast<const uint16_t*>(q);
@@ -237,8 +316,11 @@ int attn_bwd_impl(bool upload, const hydra_problem_t* p, const void* q, const vo
     a.dq = dq_acc;
     a.dk = dk_acc;
     a.dv = dv_acc;
+    a.ds = static_cast<char*>(kv_per_pass ? ds_buf : nullptr);
+    a.ds_head_bytes = int64_t(ds_head);
     const int* kitems_dev = reinterpret_cast<const int*>(static_cast<char*>(workspace) + w.kitems_off);
-    if (launch_attn_bwd(a, int(w.n_qitems), int(w.n_kitems), kitems_dev, s) != hipSuccess) return HYDRA_ERR_HIP;
+    if (launch_attn_bwd(a, int(w.n_qitems), int(w.n_kitems), kitems_dev, kv_per_pass, s) != hipSuccess)
+      return HYDRA_ERR_HIP;
     return HYDRA_OK;
   } catch (...) {
     return HYDRA_ERR_INVALID;
@@ -258,7 +340,9 @@ int hydra_attn_plan(const hydra_problem_t* p, void* workspace, size_t workspace_
     if (!workspace || workspace_bytes < w.total) return HYDRA_ERR_WORKSPACE;
     if (!aligned16(workspace)) return HYDRA_ERR_ALIGN;
     std::vector<int32_t> qitems, kitems;
-    return upload_plan(pr, w, true, workspace, static_cast<hipStream_t>(stream), &qitems, &kitems);
+    rc = upload_plan(pr, w, true, workspace, static_cast<hipStream_t>(stream), &qitems, &kitems);
+    if (rc == HYDRA_OK) record_plan(workspace, pr, true);
+    return rc;
   } catch (...) {
     return HYDRA_ERR_INVALID;
   }
@@ -277,14 +361,32 @@ int hydra_attn_fwd_planned(const hydra_problem_t* p, const void* q, const void* 
 int hydra_attn_bwd(const hydra_problem_t* p, const void* q, const void* k, const void* v, const void* o_final,
                    const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc, float* dv_acc,
                    void* workspace, size_t workspace_bytes, void* stream) {
-  return attn_bwd_impl(true, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
+  return attn_bwd_impl(true, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, nullptr, 0, workspace,
                        workspace_bytes, stream);
+}
+
+int hydra_attn_bwd_ds(const hydra_problem_t* p, const void* q, const void* k, const void* v, const void* o_final,
+                      const float* lse_final, const void* d_o, float* dq_acc, float* dk_acc, float* dv_acc,
+                      void* ds_buf, size_t ds_bytes, void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_bwd_impl(true, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, ds_buf, ds_bytes,
+                       workspace, workspace_bytes, stream);
+}
+
+size_t hydra_bwd_ds_bytes(const hydra_problem_t* p, int32_t kv_heads_per_pass) {
+  try {
+    Problem pr;
+    if (check_problem(p, &pr) != HYDRA_OK || kv_heads_per_pass < 1) return 0;
+    const uint64_t per_head = ds_bytes_per_head(pr);
+    return size_t(per_head * uint64_t(std::min(kv_heads_per_pass, pr.Hkv)) * uint64_t(pr.H / pr.Hkv));
+  } catch (...) {
+    return 0;
+  }
 }
 
 int hydra_attn_bwd_planned(const hydra_problem_t* p, const void* q, const void* k, const void* v,
                            const void* o_final, const float* lse_final, const void* d_o, float* dq_acc,
                            float* dk_acc, float* dv_acc, void* workspace, size_t workspace_bytes, void* stream) {
-  return attn_bwd_impl(false, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, workspace,
+  return attn_bwd_impl(false, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, nullptr, 0, workspace,
                        workspace_bytes, stream);
 }
 

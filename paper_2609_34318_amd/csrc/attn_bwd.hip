@@ -73,8 +73,8 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, known to the compiler
   const int m = lane & 31, hh = lane >> 5;
-  const int head = blockIdx.x % a.H;
-  const Item it(a.items, blockIdx.x / a.H);
+  const int head = a.q_head0 + blockIdx.x % a.q_heads;
+  const Item it(a.items, blockIdx.x / a.q_heads);
   const TileRanges kr = tile_ranges(it, DQ_BK);
   const int n_tiles = kr.nt;
   if (n_tiles == 0) return;  // uniform over the workgroup
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
 // P crosses from A to B through LDS (rounded to bf16, the value the dV product uses).  Per
 // 96-query tile: barrier, start the copy of the next tile (LDS holds two), phase 1 (A: S
 // and P, B: dP), barrier, phase 2 (A: dV, B: dS and dK).
-constexpr int KV_BQ = 96;                                        // query rows per tile
+constexpr int KV_BQ = KV_QTILE_ROWS;                             // query rows per tile
 constexpr int KV_NSB = KV_BQ / 32;                               // 32-row sub-blocks per tile
 constexpr int KV_VEC = 128;                                      // LDS slots per vector (LSE2, D)
 constexpr int KV_QBYTES = KV_BQ * DQK * 2;                       // 36 KB
@@ -247,6 +247,9 @@ __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, cons
   }
 }
 
+// STORE_DS: also store dS (bf16, as the MFMA operand registers hold it) for the query-
+// stationary dQ kernel that reads it back instead of recomputing S and dP.
+template <bool STORE_DS>
 __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) char smem_raw[KV_NSTAGE * KV_STAGE + KV_PBYTES];
   lds_char* smem = (lds_char*)smem_raw;
@@ -257,9 +260,10 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV   role 1: dP, dS, dK
   const int m = lane & 31, hh = lane >> 5;
   // one K/V head per workgroup; its dK/dV sum over the group's query heads head0 ..
-  const int kv_head = blockIdx.x % a.Hkv;
+  const int kv_head = a.kv_head0 + blockIdx.x % a.kv_heads;
   const int head0 = kv_head * a.grp;
-  const Item it(a.items, blockIdx.x / a.Hkv);
+  const int item_idx = blockIdx.x / a.kv_heads;
+  const Item it(a.items, item_idx);
   const TileRanges qr = tile_ranges(it, KV_BQ);
   const int n_tiles = qr.nt * a.grp;  // (query head, query tile) pairs
   if (n_tiles == 0) return;  // uniform over the workgroup
@@ -283,6 +287,8 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int ooff = dma_lane_off<DV>(a.H * DV, head0, pair, lane);
   const int poff = pair * (KV_NSB * 2048) + lane * 16;  // this lane's P slot: + sb*2048 + half*1024
   const bool active = kn_w > 0;               // uniform over the pair
+  // first dS slot of this key item (stored-dS backward only)
+  const int ds_slot0 = STORE_DS ? __builtin_amdgcn_readfirstlane(a.kbase[item_idx]) : 0;
 
   // The two roles run separate copies of the tile loop, with the same copies and the same
   // two barriers per tile: each copy keeps only its own role's operands and accumulators
@@ -428,16 +434,17 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
           });
         }
         barrier_lds();  // P of this tile is in LDS
-        // ---------------- phase 2: dS = P o (dP - D), dK^T[c][key] += Q^T[c][q] dS[q][key]
+        // ---------------- phase 2: dS = P o (dP - D) of every sub-block first (its vector
+        // work overlaps role A's dV products), then dK^T[c][key] += Q^T[c][q] dS[q][key]
         if (active) {
+          bf16x8 sf[KV_NSB][2];
           static_for<KV_BQ / 32>([&](auto sb_) {
             constexpr int sb = decltype(sb_)::value;
             bf16x8 p0, p1;
             lds_x2_bf16<2048 * sb, 2048 * sb + 1024>(pbuf, poff, p0, p1);
             f32x4 d0, d1, d2, d3;
             lds_x4_f32<KV_VEC * 4 + 128 * sb, KV_VEC * 4 + 128 * sb + 16, KV_VEC * 4 + 128 * sb + 64,
-                       KV_VEC * 4 + 128 * sb + 80>(vec_s, 32 * hh,
-                                                                                                      d0, d1, d2, d3);
+                       KV_VEC * 4 + 128 * sb + 80>(vec_s, 32 * hh, d0, d1, d2, d3);
             const float D_r[16] = {d0[0], d0[1], d0[2], d0[3], d1[0], d1[1], d1[2], d1[3],
                                    d2[0], d2[1], d2[2], d2[3], d3[0], d3[1], d3[2], d3[3]};
             float ds[16];
@@ -446,14 +453,28 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
               const float pv = (float)(e < 8 ? p0[e] : p1[e - 8]);
               ds[e] = pv * (dp[sb][e] - D_r[e]);
             }
-            const bf16x8 sf[2] = {to_bf16x8(ds), to_bf16x8(ds + 8)};
+            sf[sb][0] = to_bf16x8(ds);
+            sf[sb][1] = to_bf16x8(ds + 8);
+            if constexpr (STORE_DS) {
+              // this pair's 32 keys x sub-block sb's 32 queries, 2 KB: two 1 KB stores in the
+              // register layout (lane 32h + m: key m, queries 16*half + 8h .. +7)
+              typedef __attribute__((address_space(1))) bf16x8 gbf16x8;
+              const int member = t / qr.nt, tl = t - member * qr.nt;
+              char* dst = a.ds + (int64_t)((kv_head - a.kv_head0) * a.grp + member) * a.ds_head_bytes +
+                          (int64_t)(ds_slot0 + tl) * DS_TILE_BYTES + (sb * 4 + pair) * DS_BLOCK_BYTES + lane * 16;
+              *(gbf16x8*)(dst) = sf[sb][0];
+              *(gbf16x8*)(dst + DS_BLOCK_BYTES / 2) = sf[sb][1];
+            }
+          });
+          static_for<KV_BQ / 32>([&](auto sb_) {
+            constexpr int sb = decltype(sb_)::value;
             // groups of three Q^T column blocks
             bf16x8 f[2][3];
             op_tr_x3<KV_BQ, 32 * sb, 0>(Qs, o, f[0]);
             static_for<4>([&](auto g_) {
               constexpr int gq = decltype(g_)::value, half = gq >> 1, c0 = 3 * (gq & 1);
 #pragma unroll
-              for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], sf[half], acc[c0 + j]);
+              for (int j = 0; j < 3; ++j) acc[c0 + j] = mfma(f[gq & 1][j], sf[sb][half], acc[c0 + j]);
               if constexpr (gq + 1 < 4)
                 op_tr_x3<KV_BQ, 32 * sb + 16 * ((gq + 1) >> 1), 3 * ((gq + 1) & 1)>(Qs, o, f[(gq + 1) & 1]);
               sched_fence();
@@ -499,7 +520,192 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   else run(IntC<1>{});
 }
 
-hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems,
+// ------------------------------------------------------------------ dQ from stored dS
+// Query-stationary like bwd_dq, but reading the dS that bwd_dkdv<true> stored instead of
+// recomputing S and dP: dQ^T[c][q] += K^T[c][key] dS^T[key][q], 384 of bwd_dq's 1024 FLOP
+// per visible pair, and 2 bytes of dS read per pair (HBM-bound).  Eight waves x 32 query
+// rows; keys walk the key items that the query tile's visible ranges touch, 64 keys (half
+// an item) per tile.  Every 32-row query block coincides with one 32-row sub-block of each
+// key item's query tiling (segments are 32-aligned on this path), so a wave finds its dS
+// block from the item's ranges.
+constexpr int DQS_BK = 64;                               // keys per tile
+constexpr int DQS_KBYTES = DQS_BK * DQK * 2;             // 24 KB
+constexpr int DQS_WAVE_BYTES = 2 * DS_BLOCK_BYTES;       // a wave's 32 queries x 64 keys of dS
+constexpr int DQS_DBYTES = 8 * DQS_WAVE_BYTES;           // 32 KB
+// K tiles (mostly L2 hits) are copied one tile ahead, the dS (read once, from HBM) two
+// tiles ahead: 2 x 24 KB + 3 x 32 KB of LDS
+constexpr int DQS_KSTAGES = 2, DQS_DSTAGES = 3;
+constexpr int DQS_LDS = DQS_KSTAGES * DQS_KBYTES + DQS_DSTAGES * DQS_DBYTES;
+
+// One tile of the walk (scalars): the key item's plan entry (its query ranges), its first dS
+// slot, and which 64 of its keys.  valid = 0 once the walk is over.
+struct DsTile {
+  int valid, half, krow0, kn, slot0;
+  i32x16 item;
+};
+
+// The next 64-key tile at or after local key row r within the query item's ranges.
+__device__ __forceinline__ DsTile ds_next(const AttnArgs& a, const Item& it, int& rr, int& r) {
+  DsTile d;
+  d.valid = 0;
+  while (rr < it.nr) {
+    const int kr = rr == 0 ? it.r0 : rr == 1 ? it.r1 : rr == 2 ? it.r2 : it.r3;
+    const int kc = rr == 0 ? it.c0 : rr == 1 ? it.c1 : rr == 2 ? it.c2 : it.c3;
+    if (r < kr) r = kr;
+    if (r < kr + kc) break;
+    ++rr;
+  }
+  if (rr >= it.nr) return d;
+  const int idx = sload1(a.kmap32 + (r >> 5));
+  sload_item(a.kitems + idx * ITEM_INTS, a.kbase + idx, d.item, d.slot0);
+  d.valid = 1;
+  d.half = (r - d.item[0]) >> 6;
+  d.krow0 = d.item[0] + 64 * d.half;
+  d.kn = min(DQS_BK, d.item[2] - 64 * d.half);
+  r = d.krow0 + DQS_BK;
+  return d;
+}
+
+// Byte offset of the dS the key-stationary kernel stored for query rows [qrow, qrow + 32)
+// and the 64 keys of tile d (sub-block of the item's query tiling that holds qrow), or -1
+// when those rows do not see the item.
+__device__ __forceinline__ int64_t ds_block(const DsTile& d, int qrow) {
+  int slot = d.slot0;
+#pragma unroll
+  for (int k = 0; k < MAX_RANGES; ++k) {
+    if (k >= d.item[3]) break;
+    const int row = d.item[4 + 3 * k], cnt = d.item[6 + 3 * k];
+    if (qrow >= row && qrow < row + cnt) {
+      const int u = (qrow - row) >> 5;  // 32-row sub-block within the range
+      const int sb = u % (KV_QTILE_ROWS / 32);
+      return (int64_t)(slot + u / (KV_QTILE_ROWS / 32)) * DS_TILE_BYTES + (sb * 4 + 2 * d.half) * DS_BLOCK_BYTES;
+    }
+    slot += (cnt + KV_QTILE_ROWS - 1) / KV_QTILE_ROWS;
+  }
+  return -1;
+}
+
+__global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) char smem_raw[DQS_LDS];
+  lds_char* smem = (lds_char*)smem_raw;
+  lds_char* dsmem = smem + DQS_KSTAGES * DQS_KBYTES;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int m = lane & 31, hh = lane >> 5;
+  const int head = a.q_head0 + blockIdx.x % a.q_heads;
+  const Item it(a.items, blockIdx.x / a.q_heads);
+  int rr = 0, r = 0;
+  DsTile t0 = ds_next(a, it, rr, r);
+  if (!t0.valid) return;  // uniform over the workgroup
+  const int kv_head = head / a.grp;
+  const bool wave_rows = 32 * wave < it.n;  // the wave's 32 query rows (all valid or none)
+  const int qrow0 = it.row0 + 32 * wave;
+  const char* ds_head = a.ds + (int64_t)(head - a.q_head0) * a.ds_head_bytes;
+  const int koff = dma_lane_off<DQK>(a.k_s, kv_head, wave, lane);
+  // dS copy: LDS unit u = 4k + q8 (key k, queries 8*q8 .. +7) fetched from the stored
+  // register layout (half q8/2, lane 32*(q8%2) + k)
+  const int ds_voff = 1024 * ((lane >> 1) & 1) + 512 * (lane & 1) + 16 * (lane >> 2);
+  // transpose read of the B operand: keys 8h' + 4v + j at query 16*(g%2) + i
+  const int ds_rd = 512 * (lane >> 5) + 32 * ((lane >> 4) & 1) + 64 * ((lane >> 2) & 3) + 8 * (lane & 3);
+
+  lds_clear<512>(smem, DQS_LDS, tid);
+  __syncthreads();  // LDS cleared before the first copy lands
+
+  // copies of tile d's K rows into K stage st (every wave its share)
+  auto issue_k = [&](const DsTile& d, int st) {
+    dma_tile<DQK, DQS_BK, 8>(smem + st * DQS_KBYTES, tile_rsrc(a.k, d.krow0, d.kn, a.k_s), koff, a.k_s, wave);
+  };
+  // this wave's dS block of tile d into dS stage st; returns the copy instructions issued
+  // (0: the wave's rows do not see the tile's keys)
+  auto issue_ds = [&](const DsTile& d, int st) -> int {
+    if (!wave_rows) return 0;
+    const int64_t off = ds_block(d, qrow0);
+    if (off < 0) return 0;
+    const int bytes = d.kn > 32 ? 2 * DS_BLOCK_BYTES : DS_BLOCK_BYTES;
+    const u32x4 desc = tile_desc(ds_head, off, bytes);
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr(dsmem + st * DQS_DBYTES + wave * DQS_WAVE_BYTES));
+    dma16(m0, desc, ds_voff, 0);
+    dma16(m0 + 1024, desc, ds_voff, 256);
+    if (d.kn <= 32) return 2;
+    dma16(m0 + 2048, desc, ds_voff, 2048);
+    dma16(m0 + 3072, desc, ds_voff, 2048 + 256);
+    return 4;
+  };
+
+  f32x16 acc[DQK / 32];
+#pragma unroll
+  for (int c = 0; c < DQK / 32; ++c) acc[c] = f32x16{};
+  OperandOffsets o = operand_offsets(lane);
+
+  // issue order per wave: K(0) D(0) D(1) | K(1) D(2) | K(2) D(3) | ...: at the top of tile u
+  // only D(u+1) (issued after K(u)) may still be in flight
+  DsTile t1 = ds_next(a, it, rr, r);
+  issue_k(t0, 0);
+  int n_cur = issue_ds(t0, 0);
+  int n_1 = t1.valid ? issue_ds(t1, 1) : 0;
+  DsTile t2;
+  t2.valid = 0;
+  if (t1.valid) t2 = ds_next(a, it, rr, r);
+  for (int u = 0;; ++u) {
+    refresh(o);
+    if (n_1 == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+    else if (n_1 == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    else wait_dma();
+    barrier_lds();
+    int n_2 = 0;
+    if (t1.valid) issue_k(t1, (u + 1) % DQS_KSTAGES);
+    if (t2.valid) n_2 = issue_ds(t2, (u + 2) % DQS_DSTAGES);
+    if (n_cur > 0) {
+      const lds_char* Ks = smem + (u % DQS_KSTAGES) * DQS_KBYTES;
+      const lds_char* Ds = dsmem + (u % DQS_DSTAGES) * DQS_DBYTES + wave * DQS_WAVE_BYTES + ds_rd;
+      auto kstep = [&](auto s_) {
+        constexpr int s = decltype(s_)::value;
+        constexpr int base = 2048 * (s >> 1) + 1024 * (s & 1);
+        const bf16x8 b = join(lds_tr8(Ds + base), lds_tr8(Ds + base + 256));
+        bf16x8 f[2][3];
+        op_tr_x3<DQS_BK, 16 * s, 0>(Ks, o, f[0]);
+        op_tr_x3<DQS_BK, 16 * s, 3>(Ks, o, f[1]);
+#pragma unroll
+        for (int j = 0; j < 3; ++j) acc[j] = mfma(f[0][j], b, acc[j]);
+#pragma unroll
+        for (int j = 0; j < 3; ++j) acc[3 + j] = mfma(f[1][j], b, acc[3 + j]);
+      };
+      kstep(IntC<0>{});
+      kstep(IntC<1>{});
+      if (n_cur == 4) {
+        kstep(IntC<2>{});
+        kstep(IntC<3>{});
+      }
+    }
+    if (!t1.valid) break;
+    t1 = t2;
+    n_cur = n_1;
+    n_1 = n_2;
+    if (t2.valid) t2 = ds_next(a, it, rr, r);
+  }
+
+  if (wave_rows) {
+    float* dq = a.dq + ((int64_t)(qrow0 + m) * a.H + head) * DQK + 4 * hh;
+#pragma unroll
+    for (int c = 0; c < DQK / 32; ++c)
+#pragma unroll
+      for (int rr2 = 0; rr2 < 4; ++rr2) {
+        f32x4* p = reinterpret_cast<f32x4*>(dq + 32 * c + 8 * rr2);
+        f32x4 old = *p;
+        old[0] += a.scale * acc[c][4 * rr2];
+        old[1] += a.scale * acc[c][4 * rr2 + 1];
+        old[2] += a.scale * acc[c][4 * rr2 + 2];
+        old[3] += a.scale * acc[c][4 * rr2 + 3];
+        *p = old;
+      }
+  }
+}
+
+// kv_heads_per_pass = 0: recompute path (bwd_dq + bwd_dkdv over all heads).  Otherwise the
+// stored-dS path, in passes of that many K/V heads (the dS of one pass's query heads fits
+// a.ds): bwd_dkdv<true> stores dS, then bwd_dq_ds reads it back.
+hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const int* kitems, int kv_heads_per_pass,
                            hipStream_t stream) {
   const int64_t pairs = (int64_t)a.nq * a.H;
   const int64_t blocks = (pairs + 15) / 16 < (1 << 20) ? (pairs + 15) / 16 : (1 << 20);
@@ -509,6 +715,31 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
   prof_end(tok, stream);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (kv_heads_per_pass > 0) {
+    if (n_qitems == 0 || n_kitems == 0) return hipSuccess;
+    for (int g0 = 0; g0 < a.Hkv; g0 += kv_heads_per_pass) {
+      const int G = min(kv_heads_per_pass, a.Hkv - g0);
+      AttnArgs b = a;
+      b.items = kitems;
+      b.n_items = n_kitems;
+      b.kv_head0 = g0;
+      b.kv_heads = G;
+      b.q_head0 = g0 * a.grp;
+      b.q_heads = G * a.grp;
+      tok = prof_begin("bwd_dkdv_ds", stream);
+      hipLaunchKernelGGL(bwd_dkdv_kernel<true>, dim3(n_kitems * G), dim3(512), 0, stream, b);
+      prof_end(tok, stream);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      AttnArgs c = b;
+      c.items = a.items;
+      c.n_items = n_qitems;
+      tok = prof_begin("bwd_dq_ds", stream);
+      hipLaunchKernelGGL(bwd_dq_ds_kernel, dim3(n_qitems * G * a.grp), dim3(512), 0, stream, c);
+      prof_end(tok, stream);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   if (n_qitems > 0) {
     AttnArgs b = a;
     b.n_items = n_qitems;
@@ -523,7 +754,7 @@ hipError_t launch_attn_bwd(const AttnArgs& a, int n_qitems, int n_kitems, const 
     b.items = kitems;
     b.n_items = n_kitems;
     tok = prof_begin("bwd_dkdv", stream);
-    hipLaunchKernelGGL(bwd_dkdv_kernel, dim3(n_kitems * a.Hkv), dim3(512), 0, stream, b);
+    hipLaunchKernelGGL(bwd_dkdv_kernel<false>, dim3(n_kitems * a.Hkv), dim3(512), 0, stream, b);
     prof_end(tok, stream);
     e = hipGetLastError();
   }

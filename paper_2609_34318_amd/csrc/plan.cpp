@@ -12,6 +12,8 @@
 // (Sec. 5.1.1, Alg. 1, phase 2).
 #include "plan.h"
 
+#include "tiles.h"
+
 #include <algorithm>
 #include <cmath>
 #include <numeric>
@@ -197,6 +199,29 @@ int64_t visible_pairs(const Problem& pr) {
   return total;
 }
 
+bool ds_path_applies(const Problem& pr) {
+  if (pr.nq == 0 || pr.nk == 0) return false;
+  for (const hydra_chunk_t* c : {&pr.q, &pr.kv})
+    for (int s = 0; s < c->n_segs; ++s)
+      if (c->start[s] % 32 != 0 || c->len[s] % 32 != 0) return false;
+  return true;
+}
+
+int64_t ds_tables(const Problem& pr, const std::vector<int32_t>& kitems, std::vector<int32_t>* kbase,
+                  std::vector<int32_t>* kmap32) {
+  const int64_t n = int64_t(kitems.size()) / kItemInts;
+  kbase->assign(size_t(n), 0);
+  kmap32->assign(size_t((pr.nk + 31) / 32), -1);
+  int64_t slots = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int32_t* it = &kitems[size_t(i) * kItemInts];
+    (*kbase)[size_t(i)] = int32_t(slots);
+    for (int r = 0; r < it[3]; ++r) slots += (it[4 + 3 * r + 2] + KV_QTILE_ROWS - 1) / KV_QTILE_ROWS;
+    for (int32_t b = it[0] / 32; b < (it[0] + it[2] + 31) / 32; ++b) (*kmap32)[size_t(b)] = int32_t(i);
+  }
+  return slots;
+}
+
 WsLayout ws_layout(const Problem& pr) {
   WsLayout w{};
   const int64_t nqt = [&] {
@@ -218,6 +243,11 @@ WsLayout ws_layout(const Problem& pr) {
   off = align_up(off + size_t(nqt) * kItemInts * sizeof(int32_t), 256);
   w.kitems_off = off;
   off = align_up(off + size_t(nkt) * kItemInts * sizeof(int32_t), 256);
+  w.n_kblocks = (pr.nk + 31) / 32;
+  w.kbase_off = off;
+  off = align_up(off + size_t(nkt) * sizeof(int32_t), 256);
+  w.kmap_off = off;
+  off = align_up(off + size_t(w.n_kblocks) * sizeof(int32_t), 256);
   w.d_off = off;
   off = align_up(off + size_t(pr.H) * size_t(pr.nq) * sizeof(float), 256);
   w.lse2_off = off;

@@ -37,9 +37,20 @@ int64_t visible_pairs(const Problem& pr);
 
 // Byte offsets of the workspace regions.
 struct WsLayout {
-  size_t cu_off, qitems_off, kitems_off, d_off, lse2_off, total;
-  int64_t n_qitems, n_kitems;
+  size_t cu_off, qitems_off, kitems_off, kbase_off, kmap_off, d_off, lse2_off, total;
+  int64_t n_qitems, n_kitems, n_kblocks;
 };
 WsLayout ws_layout(const Problem& pr);
+
+// The stored-dS backward applies when every segment of both chunks starts and ends on a
+// multiple of 32 positions: the key-stationary tiles then cut the query rows into 32-row
+// blocks that coincide with the query-stationary kernel's per-wave blocks.
+bool ds_path_applies(const Problem& pr);
+
+// For the stored-dS backward, from the key items in launch order: kbase[i] = first tile
+// slot of item i (slots of 24 KB, one per query tile of the item), kmap32[b] = index of
+// the item holding local key rows [32b, 32b + 32).  Returns the slots per query head.
+int64_t ds_tables(const Problem& pr, const std::vector<int32_t>& kitems, std::vector<int32_t>* kbase,
+                  std::vector<int32_t>* kmap32);
 
 }  // namespace hydra

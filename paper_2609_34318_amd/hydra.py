@@ -95,6 +95,11 @@ def lib() -> ctypes.CDLL:
         L.hydra_attn_fwd.restype = ctypes.c_int
         L.hydra_attn_bwd.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.hydra_attn_bwd.restype = ctypes.c_int
+        L.hydra_attn_bwd_ds.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp,
+                                        ctypes.c_size_t, vp]
+        L.hydra_attn_bwd_ds.restype = ctypes.c_int
+        L.hydra_bwd_ds_bytes.argtypes = [P, ctypes.c_int32]
+        L.hydra_bwd_ds_bytes.restype = ctypes.c_size_t
         L.hydra_attn_plan.argtypes = [P, vp, ctypes.c_size_t, vp]
         L.hydra_attn_plan.restype = ctypes.c_int
         L.hydra_attn_fwd_planned.argtypes = L.hydra_attn_fwd.argtypes
@@ -240,6 +245,10 @@ def _rows(t, what: str, rows: int, heads: int, d: int) -> Tuple[Optional[int], i
         raise ValueError(f"{what}: shape {tuple(t.shape)}, expected {(rows, heads, d)}")
     if rows and (t.stride(2) != 1 or (heads > 1 and t.stride(1) != d)):
         raise ValueError(f"{what}: heads and channels must be contiguous within a token row")
+    if rows > 1 and t.stride(0) < heads * d:
+        # an expanded (broadcast) or overlapping view: the library would read rows that the
+        # allocation does not hold (a stride of 0 even means "dense" to it)
+        raise ValueError(f"{what}: token rows {t.stride(0)} elements apart overlap; at least {heads * d} needed")
     return t.data_ptr(), (t.stride(0) if rows > 1 else heads * d)
 _F32 = ("float32",)
 
@@ -297,6 +306,27 @@ def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, 
                                 _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _ptr(workspace, "workspace"),
                                 workspace.numel() * workspace.element_size(), _stream(stream)),
            "hydra_attn_bwd")
+
+
+def bwd_ds_bytes(p: Problem, kv_heads_per_pass: int) -> int:
+    """Bytes of dS scratch attn_bwd_ds needs per pass of that many K/V heads (0: the
+    stored-dS path does not apply to p)."""
+    return int(lib().hydra_bwd_ds_bytes(p.ref, kv_heads_per_pass))
+
+
+def attn_bwd_ds(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, dv_acc, ds_buf, workspace,
+                stream=None):
+    """attn_bwd with dQ from the dS the dK/dV kernel stores into ds_buf (a uint8 device
+    tensor; None or too small: the recompute path)."""
+    nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
+    qp, kp, vp = _set_rows(p, q, k, v)
+    _check(lib().hydra_attn_bwd_ds(p.ref, qp, kp, vp, _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
+                                   _ptr(lse_final, "lse_final", _F32, nqh), _ptr(d_o, "d_o", _BF16, nqh * 128),
+                                   _ptr(dq_acc, "dq_acc", _F32, nqh * 192), _ptr(dk_acc, "dk_acc", _F32, nkh * 192),
+                                   _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _ptr(ds_buf, "ds_buf"),
+                                   0 if ds_buf is None else ds_buf.numel() * ds_buf.element_size(),
+                                   _ptr(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+                                   _stream(stream)), "hydra_attn_bwd_ds")
 
 
 def lse_merge(o_acc, lse_acc, o_part, lse_part, o_bf16=None, stream=None):

@@ -29,6 +29,7 @@ class Share:
     o_tmp: Optional[torch.Tensor]
     lse_tmp: Optional[torch.Tensor]
     o_bf16: torch.Tensor
+    ds_buf: Optional[torch.Tensor] = None   # dS scratch of the stored-dS backward
 
     @property
     def nq(self) -> int:
@@ -40,15 +41,19 @@ class Share:
 
 
 def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cuda",
-               softmax_scale: float = 0.0, n_kv_heads: int = 0, graph_ready: bool = False) -> Share:
+               softmax_scale: float = 0.0, n_kv_heads: int = 0, graph_ready: bool = False,
+               ds_kv_heads: int = 0) -> Share:
     """Plans every ring step of one rank; n_kv_heads (0: n_heads) < n_heads for grouped K/V.
     graph_ready: one workspace per step, for plan() and the planned calls that a graph can
-    record."""
+    record.  ds_kv_heads > 0: the backward stores dS instead of recomputing it for dQ, in
+    passes of that many K/V heads (a dS scratch sized for the largest step), wherever the
+    stored-dS path applies."""
     probs = [hydra.Problem(cu_seqlens, n_heads, q_segs, s, softmax_scale, n_kv_heads=n_kv_heads) for s in kv_steps]
     ws = max(hydra.workspace_size(p) for p in probs)
     if ws == 0:
         raise hydra.HydraError(-1, "hydra_workspace_size")
     nq = probs[0].nq
+    ds = max(hydra.bwd_ds_bytes(p, ds_kv_heads) for p in probs) if ds_kv_heads > 0 else 0
     f32 = dict(dtype=torch.float32, device=device)
     multi = len(probs) > 1
     return Share(
@@ -61,6 +66,7 @@ def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cud
         o_tmp=torch.empty((nq, n_heads, D_V), **f32) if multi else None,
         lse_tmp=torch.empty((n_heads, nq), **f32) if multi else None,
         o_bf16=torch.empty((nq, n_heads, D_V), dtype=torch.bfloat16, device=device),
+        ds_buf=torch.empty(ds, dtype=torch.uint8, device=device) if ds > 0 else None,
     )
 
 
@@ -95,4 +101,8 @@ def backward(sh: Share, q, kv, d_o, dq: torch.Tensor, dkv: Sequence[Tuple[torch.
              planned: bool = False):
     """Accumulates dQ (over steps) and each step's dK/dV; buffers are += targets."""
     for i, (p, (k, v), (dk, dv)) in enumerate(zip(sh.problems, kv, dkv)):
-        hydra.attn_bwd(p, q, k, v, sh.o_bf16, sh.lse_acc, d_o, dq, dk, dv, _ws(sh, i, planned), planned=planned)
+        if sh.ds_buf is not None and not planned:
+            hydra.attn_bwd_ds(p, q, k, v, sh.o_bf16, sh.lse_acc, d_o, dq, dk, dv, sh.ds_buf, sh.workspace)
+        else:
+            hydra.attn_bwd(p, q, k, v, sh.o_bf16, sh.lse_acc, d_o, dq, dk, dv, _ws(sh, i, planned),
+                           planned=planned)

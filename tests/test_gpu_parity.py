@@ -31,9 +31,10 @@ def _device():
     torch.cuda.synchronize()
 
 
-def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0, Hkv=0):
-    """Forward (and backward if dO given) of a share; returns numpy results."""
-    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale, n_kv_heads=Hkv)
+def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0, Hkv=0, ds_kv_heads=0):
+    """Forward (and backward if dO given) of a share; returns numpy results.  ds_kv_heads > 0:
+    the backward stores dS for dQ (passes of that many K/V heads) where that path applies."""
+    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale, n_kv_heads=Hkv, ds_kv_heads=ds_kv_heads)
     Hk = Hkv or H
     q = dev_bf16(q_bits)
     kv = [(dev_bf16(k), dev_bf16(v)) for k, v in kv_bits]
@@ -148,6 +149,80 @@ def test_gqa_medium_forward_backward(layout, H, Hkv):
     ref = _oracle_share(cu, q_segs, steps, q, kv, do)
     _check_fwd(res, ref)
     _check_bwd(res, ref)
+
+
+# 32-aligned segments: the stored-dS backward applies (documents stay ragged)
+ALIGNED = {
+    "contiguous_1step": ([0, 300, 300, 301, 1000, 1050, 1344], [(0, 1344)], [[(0, 1344)]]),
+    "ragged_docs_3step": ([0, 300, 300, 301, 1000, 1050, 1344], [(0, 1344)],
+                          [[(0, 96)], [(96, 480), (1312, 32)], [(576, 736)]]),
+    "zigzag_2step": ([0, 1024], list(inputs.zigzag_segments(1024, 2, 0)),
+                     [list(inputs.zigzag_segments(1024, 2, 0)), list(inputs.zigzag_segments(1024, 2, 1))]),
+    "q_subset_4seg": ([0, 200, 900, 1408], [(32, 128), (832, 224), (1280, 64), (0, 32)],
+                      [[(0, 448)], [(448, 960)]]),
+}
+
+
+@pytest.mark.parametrize("dist", ["paper", "sharp", "spiky"])
+@pytest.mark.parametrize("layout", list(ALIGNED))
+def test_stored_ds_backward(layout, dist):
+    """The backward that stores dS in the dK/dV kernel and reads it back for dQ: every
+    element against the oracle, dK/dV bit-identical to the recomputing path, and dQ within
+    bf16 rounding of it; one K/V head per pass (the scratch reused across passes)."""
+    cu, q_segs, steps = ALIGNED[layout]
+    H = 3
+    q, kv, do = _gen(cu, H, q_segs, steps, dist=dist, seed=11, bwd=True)
+    for st in steps:
+        assert hydra.bwd_ds_bytes(hydra.Problem(cu, H, q_segs, st), 1) > 0
+    res = _run_share(cu, H, q_segs, steps, q, kv, do, ds_kv_heads=1)
+    ref = _oracle_share(cu, q_segs, steps, q, kv, do)
+    _check_fwd(res, ref)
+    _check_bwd(res, ref)
+    base = _run_share(cu, H, q_segs, steps, q, kv, do)
+    for (a, b), (c, d) in zip(res["dkv"], base["dkv"]):
+        assert np.array_equal(a, c) and np.array_equal(b, d)
+    assert rel_l2(res["dq"], base["dq"]) < 1e-2
+
+
+@pytest.mark.parametrize("H,Hkv,per_pass", [(8, 2, 1), (8, 2, 2), (6, 3, 2), (4, 1, 1)])
+def test_stored_ds_backward_grouped_heads(H, Hkv, per_pass):
+    """Grouped K/V heads on the stored-dS path, with passes that split the K/V heads
+    unevenly (6/3 heads in passes of 2 K/V heads leaves a last pass of 1)."""
+    cu, q_segs, steps = ALIGNED["ragged_docs_3step"]
+    q, kv, do = _gen(cu, H, q_segs, steps, dist="sharp", seed=12, bwd=True, Hkv=Hkv)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do, Hkv=Hkv, ds_kv_heads=per_pass)
+    ref = _oracle_share(cu, q_segs, steps, q, kv, do)
+    _check_fwd(res, ref)
+    _check_bwd(res, ref)
+
+
+def test_stored_ds_falls_back_where_it_does_not_apply():
+    """Unaligned segments (or no scratch): hydra_attn_bwd_ds computes exactly what
+    hydra_attn_bwd computes."""
+    cu, q_segs, steps = MEDIUM["ragged_3step"]
+    H = 2
+    p = hydra.Problem(cu, H, q_segs, steps[1])
+    assert hydra.bwd_ds_bytes(p, 1) == 0
+    q, kv, do = _gen(cu, H, q_segs, steps, dist="sharp", seed=13, bwd=True)
+    sh = ring.make_share(cu, H, q_segs, steps)
+    qd, dod = dev_bf16(q), dev_bf16(do)
+    kvd = [(dev_bf16(k), dev_bf16(v)) for k, v in kv]
+    ring.forward(sh, qd, kvd)
+    outs = []
+    for use_ds in (False, True):
+        dq = torch.zeros((sh.nq, H, D_QK), device="cuda")
+        dk = torch.zeros((kv[1][0].shape[0], H, D_QK), device="cuda")
+        dv = torch.zeros((kv[1][0].shape[0], H, D_V), device="cuda")
+        k, v = kvd[1]
+        if use_ds:
+            scratch = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+            hydra.attn_bwd_ds(p, qd, k, v, sh.o_bf16, sh.lse_acc, dod, dq, dk, dv, scratch, sh.workspace)
+        else:
+            hydra.attn_bwd(p, qd, k, v, sh.o_bf16, sh.lse_acc, dod, dq, dk, dv, sh.workspace)
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy() for t in (dq, dk, dv)])
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
 
 
 def test_gqa_rejected_when_groups_do_not_divide():
@@ -277,6 +352,16 @@ def test_binding_refuses_strided_mistyped_and_missized_tensors():
         hydra.attn_fwd(p, q.float(), q, v, o, lse, ws)
     with pytest.raises(ValueError, match="elements"):
         hydra.attn_fwd(p, q, q, v, o[:32], lse, ws)
+    # broadcast rows (token stride 0) and overlapping rows never reach the library
+    q_row = torch.zeros((1, H, D_QK), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError, match="overlap"):
+        hydra.attn_fwd(p, q_row.expand(64, H, D_QK), q, v, o, lse, ws)
+    with pytest.raises(ValueError, match="overlap"):
+        hydra.attn_fwd(p, q, q, torch.zeros((1, H, D_V), dtype=torch.bfloat16, device="cuda").expand(64, H, D_V),
+                       o, lse, ws)
+    flat = torch.zeros(64 * H * D_QK, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError, match="overlap"):
+        hydra.attn_fwd(p, q, flat.as_strided((64, H, D_QK), (D_QK, D_QK, 1)), v, o, lse, ws)
     with pytest.raises(ValueError, match="dtype"):
         hydra.pack_heads(q, torch.empty((2, 64, 1, D_QK), device="cuda"), 2)
     torch.cuda.synchronize()
@@ -356,6 +441,50 @@ def test_graph_capture_replays_match_eager():
         assert np.array_equal(dq.cpu().numpy(), eager["dq"]), rep
         for (a, b), (c, d) in zip(dkv, eager["dkv"]):
             assert np.array_equal(a.cpu().numpy(), c) and np.array_equal(b.cpu().numpy(), d), rep
+
+
+def test_planned_calls_check_which_plan_the_workspace_holds():
+    """A planned call launches on the plan in the workspace, so it is refused
+    (HYDRA_ERR_WORKSPACE, nothing launched) when the workspace's last upload was for
+    another problem, or, for the backward, was the forward's query-side items only."""
+    cu, H = [0, 300, 700], 2
+    pa = hydra.Problem(cu, H, [(0, 700)], [(0, 350)])
+    pb = hydra.Problem(cu, H, [(0, 700)], [(350, 350)])   # same sizes, other KV offsets
+    q, kv, do = _gen(cu, H, [(0, 700)], [[(0, 350)]], seed=8, bwd=True)
+    qd, kd, vd, dod = dev_bf16(q), dev_bf16(kv[0][0]), dev_bf16(kv[0][1]), dev_bf16(do)
+    ws = torch.empty(max(hydra.workspace_size(pa), hydra.workspace_size(pb)), dtype=torch.uint8, device="cuda")
+    o = torch.full((700, H, D_V), float("nan"), device="cuda")
+    lse = torch.full((H, 700), float("nan"), device="cuda")
+    hydra.attn_plan(pa, ws)
+    with pytest.raises(hydra.HydraError) as e:
+        hydra.attn_fwd(pb, qd, kd, vd, o, lse, ws, planned=True)
+    assert e.value.status == -4
+    torch.cuda.synchronize()
+    assert torch.isnan(o).all() and torch.isnan(lse).all()          # nothing was launched
+    hydra.attn_fwd(pa, qd, kd, vd, o, lse, ws, planned=True)
+    o16 = o.to(torch.bfloat16)
+    dq = torch.zeros((700, H, D_QK), device="cuda")
+    dk = torch.zeros((350, H, D_QK), device="cuda")
+    dv = torch.zeros((350, H, D_V), device="cuda")
+    hydra.attn_fwd(pb, qd, kd, vd, torch.empty_like(o), torch.empty_like(lse), ws)   # query-side plan only
+    with pytest.raises(hydra.HydraError) as e:
+        hydra.attn_bwd(pb, qd, kd, vd, o16, lse, dod, dq, dk, dv, ws, planned=True)
+    assert e.value.status == -4
+    hydra.attn_plan(pb, ws)
+    hydra.attn_plan(pa, ws)                                            # the latest upload counts
+    with pytest.raises(hydra.HydraError):
+        hydra.attn_bwd(pb, qd, kd, vd, o16, lse, dod, dq, dk, dv, ws, planned=True)
+    torch.cuda.synchronize()
+    assert dq.abs().max().item() == 0 and dk.abs().max().item() == 0 and dv.abs().max().item() == 0
+    hydra.attn_bwd(pa, qd, kd, vd, o16, lse, dod, dq, dk, dv, ws, planned=True)
+    torch.cuda.synchronize()
+    ref = oracle.attn_fwd(f32(q), f32(kv[0][0]), f32(kv[0][1]), cu, [(0, 700)], [(0, 350)])
+    assert_o_close(o.cpu().numpy(), ref[0])
+    rq, rk, rv = oracle.attn_bwd(f32(q), f32(kv[0][0]), f32(kv[0][1]), o16.float().cpu().numpy(),
+                                 lse.cpu().numpy(), f32(do), cu, [(0, 700)], [(0, 350)])
+    assert_grad_close(dq.cpu().numpy(), rq, what="dQ")
+    assert_grad_close(dk.cpu().numpy(), rk, what="dK")
+    assert_grad_close(dv.cpu().numpy(), rv, what="dV")
 
 
 def test_gradient_canaries_untouched():

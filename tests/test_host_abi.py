@@ -159,6 +159,20 @@ def test_overlapping_buffers_rejected_on_host():
     assert mg(10, 2, 128, o, lse, of, lf, lse, None) == -1                           # bf16 aliases LSE
 
 
+def test_planned_calls_refuse_an_unplanned_workspace():
+    """The planned calls launch on the plan the workspace holds; a workspace no plan was
+    uploaded into through the library is refused with HYDRA_ERR_WORKSPACE before any HIP
+    call (the addresses below are never dereferenced)."""
+    L = hydra.lib()
+    p = _problem([0, 64], 2, [(0, 64)], [(0, 64)])
+    ws = hydra.workspace_size(p)
+    M = 1 << 24
+    q, k, v, o, lse, w = (M * i for i in range(1, 7))
+    assert L.hydra_attn_fwd_planned(p.ref, q, k, v, o, lse, None, w, ws, None) == -4
+    dq, dk, dv, of, lf, do = (M * i for i in range(8, 14))
+    assert L.hydra_attn_bwd_planned(p.ref, q, k, v, of, lf, do, dq, dk, dv, w, ws, None) == -4
+
+
 def test_binding_refuses_host_tensors():
     """The library takes plain device pointers; the binding refuses a host tensor before
     any call (its address would reach a kernel)."""

@@ -20,6 +20,7 @@ from gpu_util import (TOL_GRAD, TOL_LSE, TOL_O, assert_grad_close, assert_lse_cl
 pytestmark = pytest.mark.gpu
 
 D_QK, D_V = 192, 128
+BENCH_DS = 4   # bench.py's default: stored-dS backward, 4 K/V heads per pass
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -582,7 +583,7 @@ def test_packed32k_backward_full_heads():
     w = inputs.WORKLOADS["packed32k_fwdbwd"]
     cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
     q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
-    res = _run_share(cu, H, q_segs, steps, q, kv, do)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do, ds_kv_heads=BENCH_DS)
     heads = [1, 9]
     sub = lambda x: f32(x)[:, heads]
     O, L = oracle.attn_fwd(sub(q), sub(kv[0][0]), sub(kv[0][1]), cu, q_segs, steps[0])
@@ -607,7 +608,7 @@ def test_zigzag256k_share_sampled_rows_and_tail_keys():
     w = inputs.WORKLOADS["zigzag256k_share"]
     cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
     q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
-    res = _run_share(cu, H, q_segs, steps, q, kv, do)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do, ds_kv_heads=BENCH_DS)
     heads = [2, 13]
     nq = 131072
     # query rows: head quarter, tail quarter, its last rows (which see the tail keys below)
@@ -642,7 +643,7 @@ def test_zigzag256k_uniform_closed_form_backward():
     cu, H, q_segs, steps = list(w.cu_seqlens), 2, list(w.q_segs), [list(s) for s in w.kv_steps]
     q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
     kv0 = [(np.zeros_like(k), v) for k, v in kv]
-    res = _run_share(cu, H, q_segs, steps, q, kv0, do)
+    res = _run_share(cu, H, q_segs, steps, q, kv0, do, ds_kv_heads=1)
     v_all = np.concatenate([f32(v) for _, v in kv])
     Uo, UL, n = oracle.uniform_fwd(v_all, cu, q_segs, _union(steps))
     assert_lse_close(res["lse"], UL)
@@ -652,6 +653,91 @@ def test_zigzag256k_uniform_closed_form_backward():
     dk, dv = oracle.uniform_bwd_k0(f32(q), f32(kv[1][1]), Uo, f32(do), n, cu, q_segs, steps[1], keys)
     assert_grad_close(res["dkv"][1][0][keys], dk, what="dK uniform")
     assert_grad_close(res["dkv"][1][1][keys], dv, what="dV uniform")
+
+
+def test_zigzag256k_share_dkdv_at_several_depths_and_column_sums():
+    """The benchmark share as bench.py runs it (stored-dS backward): dK/dV of the last 4096
+    keys of step 0 (positions 258048..262143, each seen by 1 to 4096 queries, all tail
+    rows) element by element at several depths, on two heads; then over all 16 heads the
+    identities that hold at any size (Sec. 2.2: rows sum over their document's keys):
+    summed over both steps' keys, sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i."""
+    w = inputs.WORKLOADS["zigzag256k_share"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
+    res = _run_share(cu, H, q_segs, steps, q, kv, do, ds_kv_heads=BENCH_DS)
+    nq = 131072
+    heads = [0, 11]
+    tail = np.arange(nq - 4096, nq)                     # positions 258048 .. 262143
+    union = [(0, 262144)]
+    k_all = f32(inputs.rows("k", union, H, D_QK))[:, heads]
+    v_all = f32(inputs.rows("v", union, H, D_V))[:, heads]
+    qh, doh = f32(q)[:, heads], f32(do)[:, heads]
+    O, L = oracle.attn_fwd(qh, k_all, v_all, cu, q_segs, union, q_rows=tail)
+    _, dk, dv = oracle.attn_bwd(qh, f32(kv[0][0])[:, heads], f32(kv[0][1])[:, heads], O, L, doh, cu, q_segs,
+                                steps[0], q_rows=tail)
+    for depth, keys in (("last 64", tail[-64:]), ("1K deep", tail[2048 - 64:2048]), ("4K deep", tail[:64]),
+                        ("sampled", tail[::97])):
+        assert_grad_close(res["dkv"][0][0][keys][:, heads], dk[keys], what=f"dK {depth}")
+        assert_grad_close(res["dkv"][0][1][keys][:, heads], dv[keys], what=f"dV {depth}")
+    dk_sum = sum(res["dkv"][i][0].astype(np.float64).sum(0) for i in range(2))    # [H, 192]
+    dv_sum = sum(res["dkv"][i][1].astype(np.float64).sum(0) for i in range(2))
+    do_sum = f32(do).astype(np.float64).sum(0)
+    for h in range(H):
+        dk_norm = np.sqrt(sum(np.linalg.norm(res["dkv"][i][0][:, h].astype(np.float64)) ** 2 for i in range(2)))
+        dv_norm = np.sqrt(sum(np.linalg.norm(res["dkv"][i][1][:, h].astype(np.float64)) ** 2 for i in range(2)))
+        assert np.linalg.norm(dk_sum[h]) <= 0.05 * dk_norm, h
+        assert np.linalg.norm(dv_sum[h] - do_sum[h]) <= 0.05 * dv_norm, h
+
+
+def test_gqa_zigzag256k_share_uniform_backward():
+    """16 query heads over 2 K/V heads at the benchmark share's size, stored-dS backward:
+    with K = 0 the softmax is uniform, dQ is exactly 0 and each K/V head's dK/dV (summed over
+    its 8 query heads, Sec. 3.5) has a closed form, checked on keys of both chunks."""
+    w = inputs.WORKLOADS["zigzag256k_share"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    Hkv = 2
+    q, kv, do = _gen(cu, H, q_segs, steps, bwd=True, Hkv=Hkv)
+    kv0 = [(np.zeros_like(k), v) for k, v in kv]
+    res = _run_share(cu, H, q_segs, steps, q, kv0, do, Hkv=Hkv, ds_kv_heads=1)
+    v_all = np.concatenate([f32(v) for _, v in kv])
+    Uo, UL, n = oracle.uniform_fwd(v_all, cu, q_segs, _union(steps), n_q_heads=H)
+    assert_lse_close(res["lse"], UL)
+    assert_o_close(res["o"], Uo)
+    assert np.abs(res["dq"]).max() == 0.0
+    for si, keys in ((0, np.array([0, 4095, 65535, 65536, 131071])), (1, np.array([0, 65535, 65536, 131071]))):
+        dk, dv = oracle.uniform_bwd_k0(f32(q), f32(kv[si][1]), Uo, f32(do), n, cu, q_segs, steps[si], keys)
+        assert_grad_close(res["dkv"][si][0][keys], dk, what=f"dK uniform step {si}")
+        assert_grad_close(res["dkv"][si][1][keys], dv, what=f"dV uniform step {si}")
+
+
+@pytest.mark.parametrize("ds", [0, 1])
+def test_head_and_document_permutations_permute_the_outputs(ds):
+    """Heads are independent and documents only see themselves: permuting the heads permutes
+    every output bit for bit (each (tile, head) runs the same code); reordering the packed
+    documents moves their rows, whose values change only by rounding (the tiles fall
+    differently), compared within the parity tolerances."""
+    cu, q_segs, steps = ALIGNED["contiguous_1step"]
+    H = 4
+    q, kv, do = _gen(cu, H, q_segs, steps, dist="sharp", seed=21, bwd=True)
+    base = _run_share(cu, H, q_segs, steps, q, kv, do, ds_kv_heads=ds)
+    perm = [2, 0, 3, 1]
+    ph = _run_share(cu, H, q_segs, steps, q[:, perm], [(k[:, perm], v[:, perm]) for k, v in kv], do[:, perm],
+                    ds_kv_heads=ds)
+    assert np.array_equal(ph["o"], base["o"][:, perm]) and np.array_equal(ph["lse"], base["lse"][perm])
+    assert np.array_equal(ph["dq"], base["dq"][:, perm])
+    assert np.array_equal(ph["dkv"][0][0], base["dkv"][0][0][:, perm])
+    assert np.array_equal(ph["dkv"][0][1], base["dkv"][0][1][:, perm])
+    lens = np.diff(cu)
+    order = [4, 1, 5, 0, 3, 2]
+    starts = np.asarray(cu)[:-1]
+    rows = np.concatenate([np.arange(starts[d], starts[d] + lens[d]) for d in order])
+    cu2 = [0] + list(np.cumsum(lens[order]))
+    pd = _run_share(cu2, H, q_segs, steps, q[rows], [(k[rows], v[rows]) for k, v in kv], do[rows], ds_kv_heads=ds)
+    assert_o_close(pd["o"], base["o"][rows])
+    assert_lse_close(pd["lse"], base["lse"][:, rows])
+    assert_grad_close(pd["dq"], base["dq"][rows], what="dQ")
+    assert_grad_close(pd["dkv"][0][0], base["dkv"][0][0][rows], what="dK")
+    assert_grad_close(pd["dkv"][0][1], base["dkv"][0][1][rows], what="dV")
 
 
 def test_offsets_past_two_to_the_31_elements():

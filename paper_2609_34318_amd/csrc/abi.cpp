@@ -118,10 +118,11 @@ int upload_plan(const Problem& pr, const WsLayout& w, bool with_kv_items, void* 
   std::memcpy(img.data() + w.qitems_off, qitems->data(), qitems->size() * sizeof(int32_t));
   if (with_kv_items) {
     std::memcpy(img.data() + w.kitems_off, kitems->data(), kitems->size() * sizeof(int32_t));
-    std::vector<int32_t> kbase, kmap32;
-    ds_tables(pr, *kitems, &kbase, &kmap32);
+    std::vector<int32_t> kbase, kmap32, krec;
+    ds_tables(pr, *kitems, &kbase, &kmap32, &krec);
     std::memcpy(img.data() + w.kbase_off, kbase.data(), kbase.size() * sizeof(int32_t));
     std::memcpy(img.data() + w.kmap_off, kmap32.data(), kmap32.size() * sizeof(int32_t));
+    std::memcpy(img.data() + w.krec_off, krec.data(), krec.size() * sizeof(int32_t));
   }
   // Pageable source: the runtime has consumed `img` when the call returns.
   if (hipMemcpyAsync(ws, img.data(), bytes, hipMemcpyHostToDevice, stream) != hipSuccess) return HYDRA_ERR_HIP;
@@ -179,6 +180,7 @@ AttnArgs base_args(const Problem& pr, const WsLayout& w, void* ws) {
   a.kitems = reinterpret_cast<const int*>(base + w.kitems_off);
   a.kbase = reinterpret_cast<const int*>(base + w.kbase_off);
   a.kmap32 = reinterpret_cast<const int*>(base + w.kmap_off);
+  a.krec = reinterpret_cast<const int*>(base + w.krec_off);
   a.n_docs = int(pr.cu.size()) - 1;
   a.H = pr.H;
   a.Hkv = pr.Hkv;
@@ -258,9 +260,9 @@ int attn_fwd_impl(bool upload, const hydra_problem_t* p, const void* q, const vo
 // Bytes of stored dS per query head on the stored-dS path (0 when the path does not apply).
 uint64_t ds_bytes_per_head(const Problem& pr) {
   if (!ds_path_applies(pr)) return 0;
-  std::vector<int32_t> kitems, kbase, kmap32;
+  std::vector<int32_t> kitems, kbase, kmap32, krec;
   plan_items(pr, 1, &kitems);
-  return uint64_t(ds_tables(pr, kitems, &kbase, &kmap32)) * DS_TILE_BYTES;
+  return uint64_t(ds_tables(pr, kitems, &kbase, &kmap32, &krec)) * DS_TILE_BYTES;
 }
 
 int attn_bwd_impl(bool upload, const hydra_problem_t* p, const void* q, const void* k, const void* v,

@@ -537,52 +537,71 @@ constexpr int DQS_DBYTES = 8 * DQS_WAVE_BYTES;           // 32 KB
 constexpr int DQS_KSTAGES = 2, DQS_DSTAGES = 3;
 constexpr int DQS_LDS = DQS_KSTAGES * DQS_KBYTES + DQS_DSTAGES * DQS_DBYTES;
 
-// One tile of the walk (scalars): the key item's plan entry (its query ranges), its first dS
-// slot, and which 64 of its keys.  valid = 0 once the walk is over.
+// One tile of the walk (scalars): 64 keys of a key item, and where the wave's dS block for
+// them sits (off < 0: the wave's rows do not see the item).  valid = 0 once the walk is over.
 struct DsTile {
-  int valid, half, krow0, kn, slot0;
-  i32x16 item;
+  int valid, krow0, kn;
+  int64_t off;
 };
 
-// The next 64-key tile at or after local key row r within the query item's ranges.
-__device__ __forceinline__ DsTile ds_next(const AttnArgs& a, const Item& it, int& rr, int& r) {
+// The walk over the key items that a query item's ranges touch, in row order, 64 keys at a
+// time.  The item records live in row order, so within a range the next item's record is
+// the next one; they are read through the constant address space, which makes them scalar
+// loads that the compiler waits for where they are used (never together with the copies in
+// flight, as vector loads after the copies' memory-clobbering assembly would be).
+struct DsWalk {
+  int rr, r, j;
+  i32x16 rec;
+};
+
+typedef const __attribute__((address_space(4))) int cint;
+typedef const __attribute__((address_space(4))) i32x16 crec16;
+
+__device__ __forceinline__ DsTile ds_next(const AttnArgs& a, const Item& it, DsWalk& w, bool wave_rows, int qrow) {
   DsTile d;
   d.valid = 0;
-  while (rr < it.nr) {
-    const int kr = rr == 0 ? it.r0 : rr == 1 ? it.r1 : rr == 2 ? it.r2 : it.r3;
-    const int kc = rr == 0 ? it.c0 : rr == 1 ? it.c1 : rr == 2 ? it.c2 : it.c3;
-    if (r < kr) r = kr;
-    if (r < kr + kc) break;
-    ++rr;
-  }
-  if (rr >= it.nr) return d;
-  const int idx = sload1(a.kmap32 + (r >> 5));
-  sload_item(a.kitems + idx * ITEM_INTS, a.kbase + idx, d.item, d.slot0);
-  d.valid = 1;
-  d.half = (r - d.item[0]) >> 6;
-  d.krow0 = d.item[0] + 64 * d.half;
-  d.kn = min(DQS_BK, d.item[2] - 64 * d.half);
-  r = d.krow0 + DQS_BK;
-  return d;
-}
-
-// Byte offset of the dS the key-stationary kernel stored for query rows [qrow, qrow + 32)
-// and the 64 keys of tile d (sub-block of the item's query tiling that holds qrow), or -1
-// when those rows do not see the item.
-__device__ __forceinline__ int64_t ds_block(const DsTile& d, int qrow) {
-  int slot = d.slot0;
-#pragma unroll
-  for (int k = 0; k < MAX_RANGES; ++k) {
-    if (k >= d.item[3]) break;
-    const int row = d.item[4 + 3 * k], cnt = d.item[6 + 3 * k];
-    if (qrow >= row && qrow < row + cnt) {
-      const int u = (qrow - row) >> 5;  // 32-row sub-block within the range
-      const int sb = u % (KV_QTILE_ROWS / 32);
-      return (int64_t)(slot + u / (KV_QTILE_ROWS / 32)) * DS_TILE_BYTES + (sb * 4 + 2 * d.half) * DS_BLOCK_BYTES;
+  bool jump = w.j < 0;
+  while (w.rr < it.nr) {
+    const int kr = w.rr == 0 ? it.r0 : w.rr == 1 ? it.r1 : w.rr == 2 ? it.r2 : it.r3;
+    const int kc = w.rr == 0 ? it.c0 : w.rr == 1 ? it.c1 : w.rr == 2 ? it.c2 : it.c3;
+    if (w.r < kr) {
+      w.r = kr;
+      jump = true;
     }
-    slot += (cnt + KV_QTILE_ROWS - 1) / KV_QTILE_ROWS;
+    if (w.r < kr + kc) break;
+    ++w.rr;
   }
-  return -1;
+  if (w.rr >= it.nr) return d;
+  if (jump) {
+    w.j = ((cint*)a.kmap32)[w.r >> 5];
+    w.rec = *(crec16*)(a.krec + w.j * ITEM_INTS);
+  } else if (w.r >= w.rec[0] + w.rec[1]) {  // past this item: the next one in row order
+    ++w.j;
+    w.rec = *(crec16*)(a.krec + w.j * ITEM_INTS);
+  }
+  const int half = (w.r - w.rec[0]) >> 6;
+  d.valid = 1;
+  d.krow0 = w.rec[0] + 64 * half;
+  d.kn = min(DQS_BK, w.rec[1] - 64 * half);
+  w.r = d.krow0 + DQS_BK;
+  // the sub-block of the item's query tiling that holds the wave's rows [qrow, qrow + 32)
+  d.off = -1;
+  if (wave_rows) {
+    int slot = w.rec[3];
+#pragma unroll
+    for (int k = 0; k < MAX_RANGES; ++k) {
+      if (k >= w.rec[2]) break;
+      const int row = w.rec[4 + 2 * k], cnt = w.rec[5 + 2 * k];
+      if (qrow >= row && qrow < row + cnt) {
+        const int u = (qrow - row) >> 5;
+        const int sb = u % (KV_QTILE_ROWS / 32);
+        d.off = (int64_t)(slot + u / (KV_QTILE_ROWS / 32)) * DS_TILE_BYTES + (sb * 4 + 2 * half) * DS_BLOCK_BYTES;
+        break;
+      }
+      slot += (cnt + KV_QTILE_ROWS - 1) / KV_QTILE_ROWS;
+    }
+  }
+  return d;
 }
 
 __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
@@ -595,12 +614,15 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
   const int m = lane & 31, hh = lane >> 5;
   const int head = a.q_head0 + blockIdx.x % a.q_heads;
   const Item it(a.items, blockIdx.x / a.q_heads);
-  int rr = 0, r = 0;
-  DsTile t0 = ds_next(a, it, rr, r);
-  if (!t0.valid) return;  // uniform over the workgroup
-  const int kv_head = head / a.grp;
   const bool wave_rows = 32 * wave < it.n;  // the wave's 32 query rows (all valid or none)
   const int qrow0 = it.row0 + 32 * wave;
+  DsWalk walk;
+  walk.rr = 0;
+  walk.r = 0;
+  walk.j = -1;
+  DsTile t0 = ds_next(a, it, walk, wave_rows, qrow0);
+  if (!t0.valid) return;  // uniform over the workgroup
+  const int kv_head = head / a.grp;
   const char* ds_head = a.ds + (int64_t)(head - a.q_head0) * a.ds_head_bytes;
   const int koff = dma_lane_off<DQK>(a.k_s, kv_head, wave, lane);
   // dS copy: LDS unit u = 4k + q8 (key k, queries 8*q8 .. +7) fetched from the stored
@@ -619,11 +641,9 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
   // this wave's dS block of tile d into dS stage st; returns the copy instructions issued
   // (0: the wave's rows do not see the tile's keys)
   auto issue_ds = [&](const DsTile& d, int st) -> int {
-    if (!wave_rows) return 0;
-    const int64_t off = ds_block(d, qrow0);
-    if (off < 0) return 0;
+    if (d.off < 0) return 0;
     const int bytes = d.kn > 32 ? 2 * DS_BLOCK_BYTES : DS_BLOCK_BYTES;
-    const u32x4 desc = tile_desc(ds_head, off, bytes);
+    const u32x4 desc = tile_desc(ds_head, d.off, bytes);
     const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr(dsmem + st * DQS_DBYTES + wave * DQS_WAVE_BYTES));
     dma16(m0, desc, ds_voff, 0);
     dma16(m0 + 1024, desc, ds_voff, 256);
@@ -640,13 +660,13 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
 
   // issue order per wave: K(0) D(0) D(1) | K(1) D(2) | K(2) D(3) | ...: at the top of tile u
   // only D(u+1) (issued after K(u)) may still be in flight
-  DsTile t1 = ds_next(a, it, rr, r);
+  DsTile t1 = ds_next(a, it, walk, wave_rows, qrow0);
   issue_k(t0, 0);
   int n_cur = issue_ds(t0, 0);
   int n_1 = t1.valid ? issue_ds(t1, 1) : 0;
   DsTile t2;
   t2.valid = 0;
-  if (t1.valid) t2 = ds_next(a, it, rr, r);
+  if (t1.valid) t2 = ds_next(a, it, walk, wave_rows, qrow0);
   for (int u = 0;; ++u) {
     refresh(o);
     if (n_1 == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
@@ -682,7 +702,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
     t1 = t2;
     n_cur = n_1;
     n_1 = n_2;
-    if (t2.valid) t2 = ds_next(a, it, rr, r);
+    if (t2.valid) t2 = ds_next(a, it, walk, wave_rows, qrow0);
   }
 
   if (wave_rows) {

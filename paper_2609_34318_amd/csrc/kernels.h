@@ -276,25 +276,7 @@ __device__ __forceinline__ void ldg_x4(const uint16_t* p, u32x4& a, u32x4& b, u3
       : "memory");
 }
 
-// A 16-int work item and one more int, at wave-uniform addresses, through the scalar cache;
-// the loads complete within the statement.  Written out because the compiler turns loads that
-// follow the copies below (whose assembly clobbers memory) into vector loads, whose waits
-// would also wait for every copy in flight.
 typedef int i32x16 __attribute__((ext_vector_type(16)));
-__device__ __forceinline__ void sload_item(const int* item, const int* word, i32x16& v, int& w) {
-  asm volatile(
-      "s_load_dwordx16 %0, %2, 0x0\n\t"
-      "s_load_dword %1, %3, 0x0\n\t"
-      "s_waitcnt lgkmcnt(0)"
-      : "=&s"(v), "=&s"(w)
-      : "s"(item), "s"(word)
-      : "memory");
-}
-__device__ __forceinline__ int sload1(const int* word) {
-  int w;
-  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=&s"(w) : "s"(word) : "memory");
-  return w;
-}
 
 // ------------------------------------------------------------------ direct global -> LDS copies
 // Copies are inline assembly, invisible to the compiler's wait insertion (see above).  A
@@ -474,12 +456,14 @@ struct AttnArgs {
   int kv_head0, kv_heads;
   int q_head0, q_heads;
   // stored-dS backward: dS blocks of the launch's query heads, ds_head_bytes apart; per key
-  // item (launch order) its first tile slot; the key item holding each 32-row key block
+  // item (launch order) its first tile slot; the key items in row order as records (row0,
+  // rows, ranges, first slot) and the record index of each 32-row key block
   char* ds;
   int64_t ds_head_bytes;
   const int* kbase;
   const int* kmap32;
-  const int* kitems;   // key-stationary items (query-stationary kernels read their ranges)
+  const int* krec;
+  const int* kitems;   // key-stationary items
 };
 
 }  // namespace hydra

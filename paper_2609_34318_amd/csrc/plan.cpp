@@ -208,16 +208,34 @@ bool ds_path_applies(const Problem& pr) {
 }
 
 int64_t ds_tables(const Problem& pr, const std::vector<int32_t>& kitems, std::vector<int32_t>* kbase,
-                  std::vector<int32_t>* kmap32) {
+                  std::vector<int32_t>* kmap32, std::vector<int32_t>* krec) {
   const int64_t n = int64_t(kitems.size()) / kItemInts;
   kbase->assign(size_t(n), 0);
   kmap32->assign(size_t((pr.nk + 31) / 32), -1);
+  krec->assign(size_t(n) * kItemInts, 0);
+  std::vector<int64_t> order(static_cast<size_t>(n));
+  std::iota(order.begin(), order.end(), int64_t(0));
+  std::sort(order.begin(), order.end(),
+            [&](int64_t x, int64_t y) { return kitems[size_t(x) * kItemInts] < kitems[size_t(y) * kItemInts]; });
   int64_t slots = 0;
   for (int64_t i = 0; i < n; ++i) {
     const int32_t* it = &kitems[size_t(i) * kItemInts];
     (*kbase)[size_t(i)] = int32_t(slots);
     for (int r = 0; r < it[3]; ++r) slots += (it[4 + 3 * r + 2] + KV_QTILE_ROWS - 1) / KV_QTILE_ROWS;
-    for (int32_t b = it[0] / 32; b < (it[0] + it[2] + 31) / 32; ++b) (*kmap32)[size_t(b)] = int32_t(i);
+  }
+  for (int64_t j = 0; j < n; ++j) {
+    const int64_t i = order[size_t(j)];
+    const int32_t* it = &kitems[size_t(i) * kItemInts];
+    int32_t* rec = &(*krec)[size_t(j) * kItemInts];
+    rec[0] = it[0];
+    rec[1] = it[2];
+    rec[2] = it[3];
+    rec[3] = (*kbase)[size_t(i)];
+    for (int r = 0; r < it[3]; ++r) {
+      rec[4 + 2 * r] = it[4 + 3 * r];
+      rec[5 + 2 * r] = it[6 + 3 * r];
+    }
+    for (int32_t b = it[0] / 32; b < (it[0] + it[2] + 31) / 32; ++b) (*kmap32)[size_t(b)] = int32_t(j);
   }
   return slots;
 }
@@ -248,6 +266,8 @@ WsLayout ws_layout(const Problem& pr) {
   off = align_up(off + size_t(nkt) * sizeof(int32_t), 256);
   w.kmap_off = off;
   off = align_up(off + size_t(w.n_kblocks) * sizeof(int32_t), 256);
+  w.krec_off = off;
+  off = align_up(off + size_t(nkt) * kItemInts * sizeof(int32_t), 256);
   w.d_off = off;
   off = align_up(off + size_t(pr.H) * size_t(pr.nq) * sizeof(float), 256);
   w.lse2_off = off;

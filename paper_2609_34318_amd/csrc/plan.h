@@ -37,7 +37,7 @@ int64_t visible_pairs(const Problem& pr);
 
 // Byte offsets of the workspace regions.
 struct WsLayout {
-  size_t cu_off, qitems_off, kitems_off, kbase_off, kmap_off, d_off, lse2_off, total;
+  size_t cu_off, qitems_off, kitems_off, kbase_off, kmap_off, krec_off, d_off, lse2_off, total;
   int64_t n_qitems, n_kitems, n_kblocks;
 };
 WsLayout ws_layout(const Problem& pr);
@@ -48,9 +48,11 @@ WsLayout ws_layout(const Problem& pr);
 bool ds_path_applies(const Problem& pr);
 
 // For the stored-dS backward, from the key items in launch order: kbase[i] = first tile
-// slot of item i (slots of 24 KB, one per query tile of the item), kmap32[b] = index of
-// the item holding local key rows [32b, 32b + 32).  Returns the slots per query head.
+// slot of item i (slots of 24 KB, one per query tile of the item); the items again in
+// row order as records of kItemInts ints, krec[j] = {row0, n, n_ranges, first slot, then
+// (first row, rows) of each query range}; kmap32[b] = the row-order index of the item
+// holding local key rows [32b, 32b + 32).  Returns the slots per query head.
 int64_t ds_tables(const Problem& pr, const std::vector<int32_t>& kitems, std::vector<int32_t>* kbase,
-                  std::vector<int32_t>* kmap32);
+                  std::vector<int32_t>* kmap32, std::vector<int32_t>* krec);
 
 }  // namespace hydra

@@ -47,6 +47,7 @@ extern "C" {
 #define HYDRA_ERR_ALIGN         -3  /* a device pointer is not 16-byte aligned */
 #define HYDRA_ERR_WORKSPACE     -4  /* workspace NULL or smaller than hydra_workspace_size() */
 #define HYDRA_ERR_HIP           -5  /* a HIP runtime call or kernel launch failed */
+#define HYDRA_ERR_TOO_LARGE     -6  /* beyond the no-allocation call's scratch (see below) */
 
 #define HYDRA_MAX_SEGS 4
 
@@ -149,6 +150,20 @@ int hydra_attn_bwd_ds(const hydra_problem_t* p, const void* q, const void* k, co
  * their query heads) per pass; 0 when `p` is invalid or the stored-dS path does not apply
  * (host only). */
 size_t hydra_bwd_ds_bytes(const hydra_problem_t* p, int32_t kv_heads_per_pass);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): hydra_attn_bwd without the workspace
+ * argument.  The workspace (plan, D, LSE*log2(e)) lives in a device array of the library,
+ * one per GPU, of hydra_noalloc_scratch_bytes() = 32 MiB, held until the process ends; the
+ * call allocates nothing.  Problems whose hydra_workspace_size() exceeds it are refused with
+ * HYDRA_ERR_TOO_LARGE before any HIP call (32 MiB covers n_heads x Nq up to about 4M, e.g.
+ * 16 heads x 256K rows).  Every call on a GPU uses that GPU's one array: calls that overlap
+ * on one GPU (other streams, other threads) race and must be serialised by the caller.
+ * Everything else (arguments, checks, results) is hydra_attn_bwd's, bit for bit. */
+int hydra_attn_bwd_noalloc(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                           const void* o_final, const float* lse_final, const void* d_o,
+                           float* dq_acc, float* dk_acc, float* dv_acc, void* stream);
+size_t hydra_noalloc_scratch_bytes(void);
 
 /* For callers that record the calls into a HIP graph (stream capture), where the plan's
  * host-to-device copy cannot be recorded: hydra_attn_plan uploads the complete work plan of

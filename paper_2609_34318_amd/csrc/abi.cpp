@@ -374,6 +374,58 @@ int hydra_attn_bwd_ds(const hydra_problem_t* p, const void* q, const void* k, co
                        workspace, workspace_bytes, stream);
 }
 
+}  // extern "C"
+
+// ------------------------------------------------------------------ the no-allocation backward
+// For callers that cannot allocate device memory (code under stream capture, tight serving
+// loops): the backward's workspace (plan, D, LSE*log2(e)) lives in this file-scope array
+// instead, one copy per GPU, held until the process ends.  Host code never passes the
+// array's name to a kernel or a copy (on the host it is only a stand-in for the symbol):
+// each device's address comes from hipGetSymbolAddress, once per device, with that device
+// current.
+namespace {
+constexpr size_t kNoAllocScratchBytes = size_t(32) << 20;  // 32 MiB
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up on its first use.
+int scratch_ptr(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return HYDRA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return HYDRA_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return HYDRA_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t hydra_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+int hydra_attn_bwd_noalloc(const hydra_problem_t* p, const void* q, const void* k, const void* v,
+                           const void* o_final, const float* lse_final, const void* d_o, float* dq_acc,
+                           float* dk_acc, float* dv_acc, void* stream) {
+  try {
+    Problem pr;
+    int rc = check_problem(p, &pr);
+    if (rc != HYDRA_OK) return rc;
+    if (ws_layout(pr).total > kNoAllocScratchBytes) return HYDRA_ERR_TOO_LARGE;
+    void* ws = nullptr;
+    if ((rc = scratch_ptr(&ws)) != HYDRA_OK) return rc;
+    return attn_bwd_impl(true, p, q, k, v, o_final, lse_final, d_o, dq_acc, dk_acc, dv_acc, nullptr, 0, ws,
+                         kNoAllocScratchBytes, stream);
+  } catch (...) {
+    return HYDRA_ERR_INVALID;
+  }
+}
+
 size_t hydra_bwd_ds_bytes(const hydra_problem_t* p, int32_t kv_heads_per_pass) {
   try {
     Problem pr;
@@ -419,6 +471,8 @@ const char* hydra_strerror(int status) {
     case HYDRA_ERR_ALIGN: return "device pointer not 16-byte aligned";
     case HYDRA_ERR_WORKSPACE: return "workspace missing or too small";
     case HYDRA_ERR_HIP: return "HIP runtime error";
+    case HYDRA_ERR_TOO_LARGE:
+      return "problem needs more workspace than the no-allocation call's 32 MiB scratch holds";
     default: return "unknown status";
   }
 }

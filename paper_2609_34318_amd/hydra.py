@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_PKG, "libhydra_attn.so")
 
 HYDRA_OK = 0
 MAX_SEGS = 4
-STATUS = {0: "ok", -1: "invalid", -2: "unsupported", -3: "align", -4: "workspace", -5: "hip"}
+STATUS = {0: "ok", -1: "invalid", -2: "unsupported", -3: "align", -4: "workspace", -5: "hip", -6: "too large"}
 
 
 class Chunk(ctypes.Structure):
@@ -100,6 +100,10 @@ def lib() -> ctypes.CDLL:
         L.hydra_attn_bwd_ds.restype = ctypes.c_int
         L.hydra_bwd_ds_bytes.argtypes = [P, ctypes.c_int32]
         L.hydra_bwd_ds_bytes.restype = ctypes.c_size_t
+        L.hydra_attn_bwd_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.hydra_attn_bwd_noalloc.restype = ctypes.c_int
+        L.hydra_noalloc_scratch_bytes.argtypes = []
+        L.hydra_noalloc_scratch_bytes.restype = ctypes.c_size_t
         L.hydra_attn_plan.argtypes = [P, vp, ctypes.c_size_t, vp]
         L.hydra_attn_plan.restype = ctypes.c_int
         L.hydra_attn_fwd_planned.argtypes = L.hydra_attn_fwd.argtypes
@@ -306,6 +310,19 @@ def attn_bwd(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, 
                                 _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _ptr(workspace, "workspace"),
                                 workspace.numel() * workspace.element_size(), _stream(stream)),
            "hydra_attn_bwd")
+
+
+def attn_bwd_noalloc(p: Problem, q, k, v, o_final_bf16, lse_final, d_o, dq_acc, dk_acc, dv_acc, stream=None):
+    """attn_bwd with the library's own per-GPU scratch as the workspace (allocates nothing;
+    calls on one GPU must not overlap)."""
+    nqh, nkh = p.nq * p.n_heads, p.nk * p.n_kv_heads
+    qp, kp, vp = _set_rows(p, q, k, v)
+    _check(lib().hydra_attn_bwd_noalloc(p.ref, qp, kp, vp, _ptr(o_final_bf16, "o_final", _BF16, nqh * 128),
+                                        _ptr(lse_final, "lse_final", _F32, nqh), _ptr(d_o, "d_o", _BF16, nqh * 128),
+                                        _ptr(dq_acc, "dq_acc", _F32, nqh * 192),
+                                        _ptr(dk_acc, "dk_acc", _F32, nkh * 192),
+                                        _ptr(dv_acc, "dv_acc", _F32, nkh * 128), _stream(stream)),
+           "hydra_attn_bwd_noalloc")
 
 
 def bwd_ds_bytes(p: Problem, kv_heads_per_pass: int) -> int:

@@ -173,6 +173,19 @@ def test_planned_calls_refuse_an_unplanned_workspace():
     assert L.hydra_attn_bwd_planned(p.ref, q, k, v, of, lf, do, dq, dk, dv, w, ws, None) == -4
 
 
+def test_noalloc_backward_checks_before_any_hip_call():
+    """The no-allocation backward rejects malformed problems (-1) and problems whose
+    workspace exceeds its 32 MiB scratch (-6) on the host; nothing is dereferenced."""
+    L = hydra.lib()
+    assert L.hydra_noalloc_scratch_bytes() == 32 << 20
+    bad = _problem([0, 100], 0, [(0, 10)], [(0, 10)])
+    assert L.hydra_attn_bwd_noalloc(bad.ref, *([None] * 10)) == -1
+    big = _problem([0, 1 << 22], 16, [(0, 1 << 22)], [(0, 256)])
+    assert hydra.workspace_size(big) > 32 << 20
+    assert L.hydra_attn_bwd_noalloc(big.ref, *([16] * 9), None) == -6
+    assert L.hydra_strerror(-6).decode().startswith("problem needs more workspace")
+
+
 def test_binding_refuses_host_tensors():
     """The library takes plain device pointers; the binding refuses a host tensor before
     any call (its address would reach a kernel)."""

@@ -73,8 +73,10 @@ __global__ __launch_bounds__(64 * DQ_WAVES, 1) void bwd_dq_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, known to the compiler
   const int m = lane & 31, hh = lane >> 5;
-  const int head = a.q_head0 + blockIdx.x % a.q_heads;
-  const Item it(a.items, blockIdx.x / a.q_heads);
+  int hl, item;
+  xcd_head_item(blockIdx.x, a.q_heads, a.n_items, hl, item);
+  const int head = a.q_head0 + hl;
+  const Item it(a.items, item);
   const TileRanges kr = tile_ranges(it, DQ_BK);
   const int n_tiles = kr.nt;
   if (n_tiles == 0) return;  // uniform over the workgroup
@@ -224,11 +226,18 @@ constexpr int KV_PBYTES = 4 * KV_NSB * 2048;                     // P: 4 pairs x
 // t while tile t+1 may stay in flight; with two, tile t's copies are the only ones in flight.
 constexpr int KV_VMCNT_ONE_TILE = (DQK / 64 + DV / 64) * (KV_BQ / 32);
 
+// The query tile of flat tile index t = member * nt + i (member: query head of the group):
+// each member's tiles are walked last first.  Every range of a key item ends where its
+// document or segment ends, which is the same row for most items, so the workgroups running
+// together start at the same query tiles and stream them through the L2 together (walked
+// first to last, they would start at their own key positions, each on its own tiles).
+__device__ __forceinline__ int kv_tile(const TileRanges& qr, int t, int member) { return qr.nt - 1 - (t - member * qr.nt); }
+
 // Flat tile index t covers (query head of the group, query tile): t = member * nt + tile.
 // wave_b: 0 .. 3, the issuing wave among the role-B waves.
 __device__ __forceinline__ void kv_issue(lds_char* smem, const AttnArgs& a, const TileRanges qr, int t, int qoff,
                                          int ooff, int head0, int wave_b, int lane) {
-  const int member = t / qr.nt, qt = t - member * qr.nt;
+  const int member = t / qr.nt, qt = kv_tile(qr, t, member);
   int row0, pos0, n;
   tile_at(qr, qt, KV_BQ, row0, pos0, n);
   lds_char* dst = smem + (t % KV_NSTAGE) * KV_STAGE;
@@ -260,9 +269,10 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
   const int pair = wave & 3, role = wave >> 2;  // role 0: S, P, dV   role 1: dP, dS, dK
   const int m = lane & 31, hh = lane >> 5;
   // one K/V head per workgroup; its dK/dV sum over the group's query heads head0 ..
-  const int kv_head = a.kv_head0 + blockIdx.x % a.kv_heads;
+  int kvl, item_idx;
+  xcd_head_item(blockIdx.x, a.kv_heads, a.n_items, kvl, item_idx);
+  const int kv_head = a.kv_head0 + kvl;
   const int head0 = kv_head * a.grp;
-  const int item_idx = blockIdx.x / a.kv_heads;
   const Item it(a.items, item_idx);
   const TileRanges qr = tile_ranges(it, KV_BQ);
   const int n_tiles = qr.nt * a.grp;  // (query head, query tile) pairs
@@ -326,7 +336,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
     for (int t = 0; t < n_tiles; ++t) {
       refresh(o);
       int q_row0, qpos, qn;
-      tile_at(qr, t % qr.nt, KV_BQ, q_row0, qpos, qn);
+      tile_at(qr, kv_tile(qr, t, t / qr.nt), KV_BQ, q_row0, qpos, qn);
       // copies of tile t are done once at most the later tiles' copies issued so far (with
       // two stages: none) are still in flight
       if constexpr (ROLE == 1) {
@@ -459,7 +469,7 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
               // this pair's 32 keys x sub-block sb's 32 queries, 2 KB: two 1 KB stores in the
               // register layout (lane 32h + m: key m, queries 16*half + 8h .. +7)
               typedef __attribute__((address_space(1))) bf16x8 gbf16x8;
-              const int member = t / qr.nt, tl = t - member * qr.nt;
+              const int member = t / qr.nt, tl = kv_tile(qr, t, member);
               char* dst = a.ds + (int64_t)((kv_head - a.kv_head0) * a.grp + member) * a.ds_head_bytes +
                           (int64_t)(ds_slot0 + tl) * DS_TILE_BYTES + (sb * 4 + pair) * DS_BLOCK_BYTES + lane * 16;
               *(gbf16x8*)(dst) = sf[sb][0];
@@ -612,8 +622,10 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int m = lane & 31, hh = lane >> 5;
-  const int head = a.q_head0 + blockIdx.x % a.q_heads;
-  const Item it(a.items, blockIdx.x / a.q_heads);
+  int hl, item;
+  xcd_head_item(blockIdx.x, a.q_heads, a.n_items, hl, item);
+  const int head = a.q_head0 + hl;
+  const Item it(a.items, item);
   const bool wave_rows = 32 * wave < it.n;  // the wave's 32 query rows (all valid or none)
   const int qrow0 = it.row0 + 32 * wave;
   DsWalk walk;

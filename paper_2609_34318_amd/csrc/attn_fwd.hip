@@ -48,8 +48,9 @@ __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a,
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, known to the compiler
   const int m = lane & 31, hh = lane >> 5;
-  const int head = blockIdx.x % a.H;
-  const Item it(a.items, blockIdx.x / a.H);
+  int head, item;
+  xcd_head_item(blockIdx.x, a.H, a.n_items, head, item);
+  const Item it(a.items, item);
   const int q_row0 = it.row0, q_pos0 = it.pos0, q_n = it.n;
   const TileRanges kr = tile_ranges(it, FWD_BK);
   const int n_tiles = kr.nt;

@@ -366,6 +366,24 @@ __device__ __forceinline__ void lds_clear(lds_char* lds, int bytes, int tid) {
     *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(lds + o) = u32x4{0u, 0u, 0u, 0u};
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup b runs on XCD b % 8), each
+// with its own L2.  When the heads of a launch are a multiple of 8, each XCD takes whole heads
+// one after another (its j-th workgroup: head (b % 8) * H / 8 + j / n_items, item j % n_items,
+// heaviest first), so the workgroups running together on an XCD stream the same head's
+// other-side tiles through its L2.  Otherwise the items of a head alternate over the XCDs
+// (head b % H, item b / H).
+constexpr int N_XCD = 8;
+__device__ __forceinline__ void xcd_head_item(int b, int n_heads, int n_items, int& head, int& item) {
+  if (n_heads % N_XCD == 0) {
+    const int x = b % N_XCD, j = b / N_XCD;
+    head = x * (n_heads / N_XCD) + j / n_items;
+    item = j % n_items;
+  } else {
+    head = b % n_heads;
+    item = b / n_heads;
+  }
+}
+
 // A work item (16 ints, see the plan), read once into scalar registers.  Plain scalar
 // members only: an array here would be placed in scratch memory and indexed dynamically.
 struct Item {

@@ -215,7 +215,7 @@ def _stats(ms):
 
 
 def measure(w, steps: int, warmup: int, kv_heads: int = 0, graph: bool = False, fwd_only: bool = False,
-            prof_steps: int = 3, copy_probe_mib: int = 0, ds_kv_heads: int = 0):
+            prof_steps: int = 3, copy_probe_mib: int = 0, ds_kv_heads: int = 0, ds_budget_gib: float = 0.0):
     """Runs one workload: warmup, a timed region of `steps` uninstrumented steps (per-step
     HIP events on the launch stream, engine clock sampled meanwhile), then `prof_steps`
     steps with the library's per-kernel timing on.  Returns the raw figures."""
@@ -247,7 +247,8 @@ def measure(w, steps: int, warmup: int, kv_heads: int = 0, graph: bool = False, 
         del src, dst
 
     sh = ring.make_share(w.cu_seqlens, H, w.q_segs, w.kv_steps, n_kv_heads=Hkv, graph_ready=graph,
-                         ds_kv_heads=0 if (graph or fwd_only) else ds_kv_heads)
+                         ds_kv_heads=0 if (graph or fwd_only) else ds_kv_heads,
+                         ds_budget_bytes=0 if (graph or fwd_only or ds_kv_heads == 0) else int(ds_budget_gib * 2**30))
     if graph:
         ring.plan(sh)
     pairs_step = [hydra.visible_pairs(p) for p in sh.problems]
@@ -295,8 +296,10 @@ def measure(w, steps: int, warmup: int, kv_heads: int = 0, graph: bool = False, 
     torch.cuda.synchronize()
     prof = hydra.profile_stop()
     ds_bytes = 0 if sh.ds_buf is None else sh.ds_buf.numel()
+    ds_heads = ring.ds_kv_heads_within(sh.problems, ds_bytes) if ds_bytes else 0
     return dict(H=H, Hkv=Hkv, nq=sh.nq, pairs_step=pairs_step, step_ms=step_ms, total_ms=total_ms, wall=wall,
-                clock=clk.summary(), prof=prof, t_gen=t_gen, tensors=(q_b, kv_b, do_b), ds_bytes=ds_bytes)
+                clock=clk.summary(), prof=prof, t_gen=t_gen, tensors=(q_b, kv_b, do_b), ds_bytes=ds_bytes,
+                ds_heads=ds_heads)
 
 
 def _kernel_tflops(st, pairs, name, prof_steps):
@@ -329,9 +332,12 @@ def main() -> int:
                     help="skip the 256K ring-step configuration (three KV chunks of 32K) timed after the headline")
     ap.add_argument("--ring-steps", type=int, default=20)
     ap.add_argument("--prof-steps", type=int, default=3, help="steps timed with per-kernel launch events")
-    ap.add_argument("--ds-kv-heads", type=int, default=4,
+    ap.add_argument("--ds-kv-heads", type=int, default=-1,
                     help="backward: K/V heads per pass of the stored-dS path (dQ from the dS the dK/dV "
-                         "kernel stores, no recompute); 0: recompute S and dP for dQ")
+                         "kernel stores, no recompute); -1: as many as fit --ds-budget-gib; 0: recompute "
+                         "S and dP for dQ")
+    ap.add_argument("--ds-budget-gib", type=float, default=72.0,
+                    help="device memory for the stored dS of one pass (of 288 GB)")
     ap.add_argument("--kv-heads", type=int, default=0,
                     help="K/V heads (grouped-query attention); 0: one per query head (MLA)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -353,7 +359,8 @@ def main() -> int:
     hydra.lib()
     w = inputs.WORKLOADS[args.workload]
     r = measure(w, args.steps, args.warmup, args.kv_heads, args.graph, prof_steps=args.prof_steps,
-                copy_probe_mib=args.copy_probe_mib, ds_kv_heads=args.ds_kv_heads)
+                copy_probe_mib=args.copy_probe_mib, ds_kv_heads=args.ds_kv_heads,
+                ds_budget_gib=args.ds_budget_gib)
     H, Hkv, pairs_step = r["H"], r["Hkv"], r["pairs_step"]
     ms_per_step = r["total_ms"] / args.steps
     pairs = sum(pairs_step) * H
@@ -392,7 +399,7 @@ def main() -> int:
                    "visible_pairs_per_head": pairs_step, "counted_tflop_per_step": round(flop_step / 1e12, 3),
                    "parallelism": PARALLELISM.get(w.name, "one rank"),
                    "launch": "hip graph replay" if args.graph else "eager",
-                   "backward": (f"stored dS, {args.ds_kv_heads} K/V heads per pass ({r['ds_bytes'] / 2**30:.1f} GiB "
+                   "backward": (f"stored dS, {r['ds_heads']} K/V heads per pass ({r['ds_bytes'] / 2**30:.1f} GiB "
                                 "scratch)") if r["ds_bytes"] else "dS recomputed for dQ"},
         "pct_of_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
         "clock": clock,
@@ -410,7 +417,8 @@ def main() -> int:
         wr = inputs.WORKLOADS["ring256k_3step"]
         ring_out = {}
         for label, fwd_only in (("fwd", True), ("fwd_bwd", False)):
-            rr = measure(wr, args.ring_steps, 3, fwd_only=fwd_only, prof_steps=2, ds_kv_heads=args.ds_kv_heads)
+            rr = measure(wr, args.ring_steps, 3, fwd_only=fwd_only, prof_steps=2,
+                         ds_kv_heads=args.ds_kv_heads, ds_budget_gib=args.ds_budget_gib)
             pr = sum(rr["pairs_step"]) * rr["H"]
             fl = pr * (FWD_FLOP_PER_PAIR + (0 if fwd_only else BWD_FLOP_PER_PAIR))
             ms = rr["total_ms"] / args.ring_steps

@@ -40,19 +40,34 @@ class Share:
         return self.problems[0].n_heads
 
 
+def ds_kv_heads_within(probs: Sequence[hydra.Problem], budget_bytes: int) -> int:
+    """The most K/V heads per pass whose stored dS fits budget_bytes in every step (0: none,
+    or the stored-dS path does not apply)."""
+    hkv = probs[0].n_kv_heads
+    best = 0
+    for g in range(1, hkv + 1):
+        need = [hydra.bwd_ds_bytes(p, g) for p in probs]
+        if max(need) == 0 or max(need) > budget_bytes:
+            break
+        best = g
+    return best
+
+
 def make_share(cu_seqlens, n_heads: int, q_segs, kv_steps: Sequence, device="cuda",
                softmax_scale: float = 0.0, n_kv_heads: int = 0, graph_ready: bool = False,
-               ds_kv_heads: int = 0) -> Share:
+               ds_kv_heads: int = 0, ds_budget_bytes: int = 0) -> Share:
     """Plans every ring step of one rank; n_kv_heads (0: n_heads) < n_heads for grouped K/V.
     graph_ready: one workspace per step, for plan() and the planned calls that a graph can
     record.  ds_kv_heads > 0: the backward stores dS instead of recomputing it for dQ, in
     passes of that many K/V heads (a dS scratch sized for the largest step), wherever the
-    stored-dS path applies."""
+    stored-dS path applies; or ds_budget_bytes > 0: as many K/V heads per pass as fit it."""
     probs = [hydra.Problem(cu_seqlens, n_heads, q_segs, s, softmax_scale, n_kv_heads=n_kv_heads) for s in kv_steps]
     ws = max(hydra.workspace_size(p) for p in probs)
     if ws == 0:
         raise hydra.HydraError(-1, "hydra_workspace_size")
     nq = probs[0].nq
+    if ds_kv_heads <= 0 and ds_budget_bytes > 0:
+        ds_kv_heads = ds_kv_heads_within(probs, ds_budget_bytes)
     ds = max(hydra.bwd_ds_bytes(p, ds_kv_heads) for p in probs) if ds_kv_heads > 0 else 0
     f32 = dict(dtype=torch.float32, device=device)
     multi = len(probs) > 1

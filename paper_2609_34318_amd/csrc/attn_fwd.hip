@@ -127,16 +127,21 @@ __global__ __launch_bounds__(64 * FWD_WAVES, 1) void attn_fwd_kernel(AttnArgs a,
           s[kb][e] = (unsigned)r < (unsigned)lim ? s[kb][e] : -INFINITY;
         }
     }
-    // row max as a tree of independent chains (short dependency chains)
+    // row max as four independent chains that take two new values per step (one
+    // three-input maximum each)
     float mx4[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const f32x16& v = s[j >> 1];
       const int e0 = 8 * (j & 1);
-      mx4[j] = fmax2(fmax2(fmax2(v[e0], v[e0 + 1]), fmax2(v[e0 + 2], v[e0 + 3])),
-                     fmax2(fmax2(v[e0 + 4], v[e0 + 5]), fmax2(v[e0 + 6], v[e0 + 7])));
+      float t = fmax2(fmax2(v[e0], v[e0 + 1]), v[e0 + 2]);
+      t = fmax2(fmax2(t, v[e0 + 3]), v[e0 + 4]);
+      mx4[j] = fmax2(fmax2(t, v[e0 + 5]), v[e0 + 6]);
     }
-    const float mx = fmax2(fmax2(mx4[0], mx4[1]), fmax2(mx4[2], mx4[3]));
+    float mx = fmax2(fmax2(mx4[0], s[0][7]), s[0][15]);
+    mx = fmax2(fmax2(mx, mx4[1]), s[1][7]);
+    mx = fmax2(fmax2(mx, mx4[2]), s[1][15]);
+    mx = fmax2(mx, mx4[3]);
     const float mxs = xhalf_max(mx) * sl2;  // -inf when nothing is visible
     if (__builtin_amdgcn_ballot_w64(mxs > m_run + RESCALE_SLACK) != 0) {
       const float m_new = mxs > m_run + RESCALE_SLACK ? mxs : m_run;

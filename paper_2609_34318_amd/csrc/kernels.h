@@ -46,7 +46,9 @@ __device__ __forceinline__ f32x16 mfma(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float fmax2(float a, float b) { return __builtin_fmaxf(a, b); }
+// IEEE 754-2019 maximum (a NaN operand gives NaN; scores never are NaN).  Unlike fmax it
+// needs no canonicalising v_max of each operand first: nested calls become v_maximum3_f32.
+__device__ __forceinline__ float fmax2(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 
 // Value held by the lane 32 positions away (m stays, h flips) and the max / sum with it.
 __device__ __forceinline__ float xhalf_max(float v) {

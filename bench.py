@@ -163,40 +163,77 @@ def host_info() -> dict:
             "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
 
 
-def cpu_baseline(w, q, kv, do, budget_rows: int):
-    """The fp64 oracle on a bounded sample of the same workload: one head, the last
-    `budget_rows` query rows (the longest rows of the share), forward over all ring steps
-    and the backward of every step.  Returns counted TFLOP/s and what was sampled."""
+def _oracle_pass(w, q, kv, do, heads, rows):
+    """The oracle's forward over all ring steps (and, for a training workload, the backward
+    of every step) for the given heads and query rows; returns (visible pairs x heads,
+    counted FLOP, seconds)."""
     import numpy as np
-    from threadpoolctl import threadpool_info
 
     import oracle
     from paper_2609_34318_amd import inputs
 
     f = inputs.bf16_bits_to_f32
-    head = [0]
-    nq = q.shape[0]
-    rows = np.arange(nq - budget_rows, nq)
     union = [seg for s in w.kv_steps for seg in s]
-    qh, doh = f(q[:, head]), f(do[:, head])
-    k_all = np.concatenate([f(k[:, head]) for k, _ in kv])
-    v_all = np.concatenate([f(v[:, head]) for _, v in kv])
+    qh = f(q[:, heads])
+    k_all = np.concatenate([f(k[:, heads]) for k, _ in kv])
+    v_all = np.concatenate([f(v[:, heads]) for _, v in kv])
     qpos = oracle.row_positions(w.q_segs)[rows]
-    pairs = sum(oracle.visible_pairs_bruteforce(list(w.cu_seqlens), [(int(p), 1) for p in qpos], list(s))
-                for s in w.kv_steps)
+    pairs = len(heads) * sum(oracle.visible_pairs_bruteforce(list(w.cu_seqlens), [(int(p), 1) for p in qpos],
+                                                             list(s)) for s in w.kv_steps)
     t0 = time.perf_counter()
     O, L = oracle.attn_fwd(qh, k_all, v_all, list(w.cu_seqlens), list(w.q_segs), union, q_rows=rows)
-    for s, (k, v) in zip(w.kv_steps, kv):
-        oracle.attn_bwd(qh, f(k[:, head]), f(v[:, head]), O, L, doh, list(w.cu_seqlens), list(w.q_segs),
-                        list(s), q_rows=rows)
+    if do is not None:
+        doh = f(do[:, heads])
+        for s, (k, v) in zip(w.kv_steps, kv):
+            oracle.attn_bwd(qh, f(k[:, heads]), f(v[:, heads]), O, L, doh, list(w.cu_seqlens), list(w.q_segs),
+                            list(s), q_rows=rows)
     dt = time.perf_counter() - t0
+    flops = pairs * (FWD_FLOP_PER_PAIR + (BWD_FLOP_PER_PAIR if do is not None else 0))
+    return pairs, flops, dt
+
+
+def cpu_baseline(w, q, kv, do, budget_rows: int, heads=(0,), one_core_rows: int = -1):
+    """The fp64 oracle on a bounded sample of the same workload: the given heads, the last
+    `budget_rows` query rows (the longest rows of the share), forward over all ring steps
+    and the backward of every step, with the host's BLAS threads; then the last
+    `one_core_rows` rows (default budget_rows / 8) with one thread.  Returns counted
+    TFLOP/s and what was sampled."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    nq = q.shape[0]
+    heads = list(heads)
+    budget_rows = min(budget_rows, nq)
+    pairs, flops, dt = _oracle_pass(w, q, kv, do, heads, np.arange(nq - budget_rows, nq))
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("internal_api") in
                    ("openblas", "mkl", "blis")] or [1])
-    flops = pairs * (FWD_FLOP_PER_PAIR + BWD_FLOP_PER_PAIR)
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"1 of {w.n_heads} heads, last {budget_rows} of {nq} query rows, forward over "
-                      f"both ring steps + backward of each step ({pairs} visible pairs, {dt:.1f} s)",
-            "host": host_info()}
+    what = "forward over all ring steps" + (" + backward of each step" if do is not None else "")
+    out = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+           "sample": f"{len(heads)} of {w.n_heads} heads, last {budget_rows} of {nq} query rows, {what} "
+                     f"({pairs} visible pairs, {dt:.1f} s)",
+           "host": host_info()}
+    one = budget_rows // 8 if one_core_rows < 0 else min(one_core_rows, nq)
+    if one > 0:
+        with threadpool_limits(limits=1):
+            p1, f1, d1 = _oracle_pass(w, q, kv, do, heads, np.arange(nq - one, nq))
+        out["one_core"] = {"value": f1 / d1 / 1e12, "cores": 1,
+                           "sample": f"last {one} query rows, same heads ({p1} visible pairs, {d1:.1f} s)"}
+    return out
+
+
+def oracle_timings(cpu_rows: int) -> int:
+    """Oracle timings on every workload (host only, no GPU): the small two-step share whole
+    (all heads and rows), the others on the bounded sample the bench line uses."""
+    from paper_2609_34318_amd import inputs
+
+    for name, w in inputs.WORKLOADS.items():
+        q, kv, do = inputs.make_tensors(w)
+        whole = q.shape[0] * w.n_heads <= 4096
+        heads = range(w.n_heads) if whole else (0,)
+        rows = q.shape[0] if whole else cpu_rows
+        rec = cpu_baseline(w, q, kv, do, rows, heads=heads, one_core_rows=rows if whole else -1)
+        print(json.dumps({"workload": name, "whole": whole, **rec}), flush=True)
+    return 0
 
 
 # What share of a context-parallel group each workload is (its heads are h / cp_u).
@@ -328,6 +365,9 @@ def main() -> int:
     ap.add_argument("--workload", default="zigzag256k_share")
     ap.add_argument("--cpu-rows", type=int, default=2048, help="query rows in the oracle timing sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--oracle-timings", action="store_true",
+                    help="host only: time the oracle on every workload (the small share whole, the others "
+                         "on the --cpu-rows sample), with the host's threads and with one; no GPU is used")
     ap.add_argument("--no-ring-config", action="store_true",
                     help="skip the 256K ring-step configuration (three KV chunks of 32K) timed after the headline")
     ap.add_argument("--ring-steps", type=int, default=20)
@@ -346,6 +386,8 @@ def main() -> int:
                     help="plan once, record one step into a HIP graph and time its replays "
                          "(per-kernel times then come from eager steps of the same calls)")
     args = ap.parse_args()
+    if args.oracle_timings:
+        return oracle_timings(args.cpu_rows)
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
               "run with --gpus 1", file=sys.stderr)

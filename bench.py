@@ -132,12 +132,20 @@ class ClockSampler:
         self._stop.set()
         self._thread.join(timeout=15)
 
+    MIN_SAMPLES = 5
+
     def summary(self):
+        """Mean, median and range of the samples; `held_mhz` (the median) is what the
+        "% of peak at the measured clock" uses, and is None when the timed region was too
+        short for MIN_SAMPLES readings (a reading can then be the idle clock before the
+        work ramps up)."""
         if not self.mhz:
             return None
         import statistics
+        med = statistics.median(self.mhz)
         out = {"source": self.source, "samples": len(self.mhz), "mean_mhz": round(statistics.fmean(self.mhz), 1),
-               "min_mhz": min(self.mhz), "max_mhz": max(self.mhz)}
+               "median_mhz": med, "min_mhz": min(self.mhz), "max_mhz": max(self.mhz),
+               "held_mhz": med if len(self.mhz) >= self.MIN_SAMPLES else None}
         if self.watts:
             out["mean_w"] = round(statistics.fmean(self.watts), 1)
         return out
@@ -419,7 +427,8 @@ def main() -> int:
     clock = r["clock"]
     if clock:
         # the same rate against the dense peak at the engine clock held during the timed region
-        clock["pct_of_peak_at_measured_clock"] = round(100 * value / (PEAK_BF16_TFLOPS * clock["mean_mhz"] / 2400), 2)
+        clock["pct_of_peak_at_measured_clock"] = (
+            round(100 * value / (PEAK_BF16_TFLOPS * clock["held_mhz"] / 2400), 2) if clock["held_mhz"] else None)
 
     out = {
         "metric": "causal attention TFLOP/s fwd+bwd per rank; % of MI355X bf16 MFMA peak",
@@ -469,9 +478,12 @@ def main() -> int:
                    "pct_of_peak": round(100 * v / PEAK_BF16_TFLOPS, 2), "counted_tflop_per_step": round(fl / 1e12, 3),
                    "kernels": {k: round(x["avg_ms"], 4) for k, x in rr["prof"].items()}}
             if rr["clock"]:
+                held = rr["clock"]["held_mhz"]
                 rec["clock_mean_mhz"] = rr["clock"]["mean_mhz"]
-                rec["pct_of_peak_at_measured_clock"] = round(
-                    100 * v / (PEAK_BF16_TFLOPS * rr["clock"]["mean_mhz"] / 2400), 2)
+                rec["clock_held_mhz"] = held
+                rec["clock_samples"] = rr["clock"]["samples"]
+                rec["pct_of_peak_at_measured_clock"] = (
+                    round(100 * v / (PEAK_BF16_TFLOPS * held / 2400), 2) if held else None)
             ring_out[label] = rec
         out["ring256k_3step"] = {"steps": args.ring_steps, "visible_pairs_per_head": rr["pairs_step"],
                                  **ring_out}

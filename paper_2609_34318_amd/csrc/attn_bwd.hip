@@ -467,13 +467,14 @@ __global__ __launch_bounds__(512, 1) void bwd_dkdv_kernel(AttnArgs a) {
             sf[sb][1] = to_bf16x8(ds + 8);
             if constexpr (STORE_DS) {
               // this pair's 32 keys x sub-block sb's 32 queries, 2 KB: two 1 KB stores in the
-              // register layout (lane 32h + m: key m, queries 16*half + 8h .. +7)
-              typedef __attribute__((address_space(1))) bf16x8 gbf16x8;
+              // register layout (lane 32h + m: key m, queries 16*half + 8h .. +7), non-temporal
+              // (read once, by the dQ kernel)
+              typedef __attribute__((address_space(1))) u32x4 gu32x4;
               const int member = t / qr.nt, tl = kv_tile(qr, t, member);
               char* dst = a.ds + (int64_t)((kv_head - a.kv_head0) * a.grp + member) * a.ds_head_bytes +
                           (int64_t)(ds_slot0 + tl) * DS_TILE_BYTES + (sb * 4 + pair) * DS_BLOCK_BYTES + lane * 16;
-              *(gbf16x8*)(dst) = sf[sb][0];
-              *(gbf16x8*)(dst + DS_BLOCK_BYTES / 2) = sf[sb][1];
+              __builtin_nontemporal_store(__builtin_bit_cast(u32x4, sf[sb][0]), (gu32x4*)(dst));
+              __builtin_nontemporal_store(__builtin_bit_cast(u32x4, sf[sb][1]), (gu32x4*)(dst + DS_BLOCK_BYTES / 2));
             }
           });
           static_for<KV_BQ / 32>([&](auto sb_) {
@@ -657,11 +658,11 @@ __global__ __launch_bounds__(512, 1) void bwd_dq_ds_kernel(AttnArgs a) {
     const int bytes = d.kn > 32 ? 2 * DS_BLOCK_BYTES : DS_BLOCK_BYTES;
     const u32x4 desc = tile_desc(ds_head, d.off, bytes);
     const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_addr(dsmem + st * DQS_DBYTES + wave * DQS_WAVE_BYTES));
-    dma16(m0, desc, ds_voff, 0);
-    dma16(m0 + 1024, desc, ds_voff, 256);
+    dma16_stream(m0, desc, ds_voff, 0);
+    dma16_stream(m0 + 1024, desc, ds_voff, 256);
     if (d.kn <= 32) return 2;
-    dma16(m0 + 2048, desc, ds_voff, 2048);
-    dma16(m0 + 3072, desc, ds_voff, 2048 + 256);
+    dma16_stream(m0 + 2048, desc, ds_voff, 2048);
+    dma16_stream(m0 + 3072, desc, ds_voff, 2048 + 256);
     return 4;
   };
 

@@ -315,6 +315,19 @@ __device__ __forceinline__ void dma16(uint32_t m0v, u32x4 desc, int voff, int in
       : "s"(inc), "v"(voff), "s"(m0v), "s"(desc)
       : "memory", "m0");
 }
+// dma16 for bytes read exactly once (the stored dS): the non-temporal hint keeps them from
+// displacing lines that other workgroups read again (the K tiles of the same head).
+__device__ __forceinline__ void dma16_stream(uint32_t m0v, u32x4 desc, int voff, int inc) {
+  int tmp;
+  asm volatile(
+      "v_add_u32 %0, %1, %2\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 4\n\t"
+      "buffer_load_dwordx4 %0, %4, 0 offen nt lds"
+      : "=&v"(tmp)
+      : "s"(inc), "v"(voff), "s"(m0v), "s"(desc)
+      : "memory", "m0");
+}
 __device__ __forceinline__ void dma4(uint32_t m0v, u32x4 desc, int voff) {
   asm volatile(
       "s_mov_b32 m0, %1\n\t"

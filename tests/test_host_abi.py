@@ -315,3 +315,46 @@ def test_visible_pairs_of_the_workloads():
         assert got == counts, name
     # the packed microbatch: sum of s(s+1)/2 over its documents
     assert 144931409 == sum(s * (s + 1) // 2 for s in inputs.PACKED32K_DOCS)
+
+
+def test_stored_ds_bytes_and_the_budget_choice():
+    """The dS buffer of the stored-dS backward: per query head it holds every visible pair
+    (2 bytes each) in 24 KB slots, so at least 2 bytes per pair and at most the slots that
+    the pairs touch; the pass size bench.py picks is the most K/V heads that fit a budget;
+    a problem with a segment off the 32-row grid gets no dS buffer (recompute path)."""
+    from paper_2609_34318_amd import ring
+    w = inputs.WORKLOADS["zigzag256k_share"]
+    probs = [hydra.Problem(w.cu_seqlens, w.n_heads, w.q_segs, s) for s in w.kv_steps]
+    for p in probs:
+        one = hydra.bwd_ds_bytes(p, 1)
+        assert one % (24 * 1024) == 0
+        assert 2 * hydra.visible_pairs(p) <= one <= 2 * hydra.visible_pairs(p) * 1.01
+        assert hydra.bwd_ds_bytes(p, 4) == 4 * one
+    need4 = max(hydra.bwd_ds_bytes(p, 4) for p in probs)
+    assert ring.ds_kv_heads_within(probs, 72 << 30) == 4
+    assert ring.ds_kv_heads_within(probs, need4) == 4
+    assert ring.ds_kv_heads_within(probs, need4 - 1) == 3
+    assert ring.ds_kv_heads_within(probs, 0) == 0
+    packed = inputs.WORKLOADS["packed32k_fwdbwd"]
+    pp = [hydra.Problem(packed.cu_seqlens, packed.n_heads, packed.q_segs, s) for s in packed.kv_steps]
+    assert ring.ds_kv_heads_within(pp, 72 << 30) == 16
+    ragged = hydra.Problem([0, 100, 300], 4, [(0, 300)], [(0, 300)])
+    assert hydra.bwd_ds_bytes(ragged, 1) == 0
+    assert ring.ds_kv_heads_within([ragged], 72 << 30) == 0
+
+
+def test_oracle_timings_run_on_the_host():
+    """bench.py --oracle-timings times the oracle on every workload without a GPU: one JSON
+    line each, the small share whole, every line with a one-thread figure."""
+    import json
+    import subprocess
+    import sys
+    env = dict(os.environ, HIP_VISIBLE_DEVICES="", CUDA_VISIBLE_DEVICES="")
+    out = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--oracle-timings", "--cpu-rows", "64"],
+                         capture_output=True, text=True, timeout=600, env=env, check=True).stdout
+    recs = [json.loads(line) for line in out.splitlines() if line.startswith("{")]
+    assert [r["workload"] for r in recs] == list(inputs.WORKLOADS)
+    for r in recs:
+        assert r["value"] > 0 and r["one_core"]["value"] > 0 and r["one_core"]["cores"] == 1
+        assert r["whole"] == (r["workload"] == "tiny_2step")
+        assert r["host"]["nproc"] >= 1

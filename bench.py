@@ -453,6 +453,10 @@ def main() -> int:
                    "backward": (f"stored dS, {r['ds_heads']} K/V heads per pass ({r['ds_bytes'] / 2**30:.1f} GiB "
                                 "scratch)") if r["ds_bytes"] else "dS recomputed for dQ"},
         "pct_of_peak": round(100 * value / PEAK_BF16_TFLOPS, 2),
+        "flop_note": {"counted_per_pair": {"fwd": FWD_FLOP_PER_PAIR, "bwd": BWD_FLOP_PER_PAIR},
+                      "bwd_without_s_recompute": BWD_FLOP_PER_PAIR - 2 * D_QK,
+                      "value_without_s_recompute": round(value * (FWD_FLOP_PER_PAIR + BWD_FLOP_PER_PAIR - 2 * D_QK)
+                                                         / (FWD_FLOP_PER_PAIR + BWD_FLOP_PER_PAIR), 2)},
         "clock": clock,
         "kernels": kernels,
         "kernel_timing": f"library launch events over {args.prof_steps} further eager steps; tflops_executed "

@@ -45,9 +45,24 @@ def rel_l2(got, ref) -> float:
     return float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
 
 
+def worst_head_rel_l2(got, ref):
+    """Largest per-head relative L2 of [rows, heads, dim] tensors (None for other shapes)."""
+    got, ref = np.asarray(got, dtype=np.float64), np.asarray(ref, dtype=np.float64)
+    if got.ndim != 3 or got.shape != ref.shape:
+        return None
+    worst = 0.0
+    for h in range(got.shape[1]):
+        n = np.linalg.norm(ref[:, h])
+        if n > 0:
+            worst = max(worst, np.linalg.norm(got[:, h] - ref[:, h]) / n)
+    return worst
+
+
 def assert_grad_close(got, ref, tol=TOL_GRAD, what="grad"):
+    """Relative L2 over the whole tensor (all heads) within tol; the message also names the
+    worst head's relative L2."""
     got = np.asarray(got, dtype=np.float64)
     assert np.isfinite(got).all(), f"{what}: non-finite values"
     e = rel_l2(got, ref)
-    assert e <= tol, f"{what}: relative L2 {e:.3e} > {tol}"
+    assert e <= tol, f"{what}: relative L2 {e:.3e} > {tol} (worst head {worst_head_rel_l2(got, ref)})"
     return e

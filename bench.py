@@ -57,8 +57,10 @@ def _source_sha(kernel: str) -> str:
     return h.hexdigest()[:16]
 
 
-def _traffic(kernel: str, workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if still current."""
+def _traffic(kernel: str, workload: str, ds_heads: int = 0):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if still current
+    (same kernel code; for the stored-dS kernels also the same K/V heads per pass, since a
+    launch covers one pass)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as f:
@@ -66,6 +68,8 @@ def _traffic(kernel: str, workload: str):
     except (OSError, KeyError, ValueError):
         return None
     if rec.get("source_sha") != _source_sha(kernel):
+        return None
+    if kernel.endswith("_ds") and rec.get("kv_heads_per_pass") != ds_heads:
         return None
     return rec.get("bytes_per_launch")
 
@@ -424,7 +428,7 @@ def main() -> int:
     achieved = _kernel_tflops(prof[dom], pairs, dom, args.prof_steps)
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": _traffic(dom, w.name)}
+                "traffic": _traffic(dom, w.name, r["ds_heads"])}
     clock = r["clock"]
     if clock:
         # the same rate against the dense peak at the engine clock held during the timed region

@@ -388,9 +388,9 @@ def main() -> int:
                     help="backward: K/V heads per pass of the stored-dS path (dQ from the dS the dK/dV "
                          "kernel stores, no recompute); -1: as many as fit --ds-budget-gib; 0: recompute "
                          "S and dP for dQ")
-    ap.add_argument("--ds-budget-gib", type=float, default=18.0,
-                    help="device memory for the stored dS of one pass (of 288 GB); smaller passes measured "
-                         "faster on the 128K share (one K/V head, 16 GiB, against four, 64 GiB)")
+    ap.add_argument("--ds-budget-gib", type=float, default=None,
+                    help="device memory for the stored dS of one pass (of 288 GB); default: the library's "
+                         "(18 GiB: one K/V head per pass on the 128K share, measured faster than four)")
     ap.add_argument("--kv-heads", type=int, default=0,
                     help="K/V heads (grouped-query attention); 0: one per query head (MLA)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -412,6 +412,9 @@ def main() -> int:
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     hydra.lib()
+    if args.ds_budget_gib is None:
+        from paper_2609_34318_amd import ring
+        args.ds_budget_gib = ring.DEFAULT_DS_BUDGET_BYTES / 2**30
     w = inputs.WORKLOADS[args.workload]
     r = measure(w, args.steps, args.warmup, args.kv_heads, args.graph, prof_steps=args.prof_steps,
                 copy_probe_mib=args.copy_probe_mib, ds_kv_heads=args.ds_kv_heads,

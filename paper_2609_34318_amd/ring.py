@@ -40,6 +40,11 @@ class Share:
         return self.problems[0].n_heads
 
 
+# Device memory for the stored dS of one backward pass: on the 128K zigzag share one K/V
+# head per pass (16 GiB) measured faster than four (64 GiB).
+DEFAULT_DS_BUDGET_BYTES = 18 << 30
+
+
 def ds_kv_heads_within(probs: Sequence[hydra.Problem], budget_bytes: int) -> int:
     """The most K/V heads per pass whose stored dS fits budget_bytes in every step (0: none,
     or the stored-dS path does not apply)."""

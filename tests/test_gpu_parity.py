@@ -20,7 +20,7 @@ from gpu_util import (TOL_GRAD, TOL_LSE, TOL_O, assert_grad_close, assert_lse_cl
 pytestmark = pytest.mark.gpu
 
 D_QK, D_V = 192, 128
-BENCH_DS = 4   # bench.py's default: stored-dS backward, 4 K/V heads per pass
+BENCH_DS = -1  # bench.py's default: stored-dS backward, passes sized to ring.DEFAULT_DS_BUDGET_BYTES
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -34,8 +34,11 @@ def _device():
 
 def _run_share(cu, H, q_segs, steps, q_bits, kv_bits, do_bits=None, scale=0.0, Hkv=0, ds_kv_heads=0):
     """Forward (and backward if dO given) of a share; returns numpy results.  ds_kv_heads > 0:
-    the backward stores dS for dQ (passes of that many K/V heads) where that path applies."""
-    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale, n_kv_heads=Hkv, ds_kv_heads=ds_kv_heads)
+    the backward stores dS for dQ (passes of that many K/V heads) where that path applies;
+    BENCH_DS: passes as bench.py sizes them by default."""
+    budget = ring.DEFAULT_DS_BUDGET_BYTES if ds_kv_heads == BENCH_DS else 0
+    sh = ring.make_share(cu, H, q_segs, steps, softmax_scale=scale, n_kv_heads=Hkv, ds_kv_heads=ds_kv_heads,
+                         ds_budget_bytes=budget)
     Hk = Hkv or H
     q = dev_bf16(q_bits)
     kv = [(dev_bf16(k), dev_bf16(v)) for k, v in kv_bits]

@@ -338,6 +338,9 @@ def test_stored_ds_bytes_and_the_budget_choice():
     packed = inputs.WORKLOADS["packed32k_fwdbwd"]
     pp = [hydra.Problem(packed.cu_seqlens, packed.n_heads, packed.q_segs, s) for s in packed.kv_steps]
     assert ring.ds_kv_heads_within(pp, 72 << 30) == 16
+    # the default budget: one K/V head per pass on the share, one pass on the packed batch
+    assert ring.ds_kv_heads_within(probs, ring.DEFAULT_DS_BUDGET_BYTES) == 1
+    assert ring.ds_kv_heads_within(pp, ring.DEFAULT_DS_BUDGET_BYTES) == 16
     ragged = hydra.Problem([0, 100, 300], 4, [(0, 300)], [(0, 300)])
     assert hydra.bwd_ds_bytes(ragged, 1) == 0
     assert ring.ds_kv_heads_within([ragged], 72 << 30) == 0

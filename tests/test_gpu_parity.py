@@ -713,6 +713,29 @@ def test_gqa_zigzag256k_share_uniform_backward():
         assert_grad_close(res["dkv"][si][1][keys], dv, what=f"dV uniform step {si}")
 
 
+def test_ring256k_3step_uniform_backward_as_benchmarked():
+    """The 256K ring configuration (32K query chunk against three 32K KV chunks: the own
+    chunk, a fully visible one, a fully masked one) with the backward bench.py times on it
+    (stored dS, passes sized by the default budget): with K = 0 the softmax is uniform, so
+    O, LSE, dQ (exactly 0) and the dK/dV of sampled keys of every step have closed forms;
+    the masked step's dK/dV stay exactly zero."""
+    w = inputs.WORKLOADS["ring256k_3step"]
+    cu, H, q_segs, steps = list(w.cu_seqlens), w.n_heads, list(w.q_segs), [list(s) for s in w.kv_steps]
+    q, kv, do = _gen(cu, H, q_segs, steps, bwd=True)
+    kv0 = [(np.zeros_like(k), v) for k, v in kv]
+    res = _run_share(cu, H, q_segs, steps, q, kv0, do, ds_kv_heads=BENCH_DS)
+    v_all = np.concatenate([f32(v) for _, v in kv])
+    Uo, UL, n = oracle.uniform_fwd(v_all, cu, q_segs, _union(steps))
+    assert_lse_close(res["lse"], UL)
+    assert_o_close(res["o"], Uo)
+    assert np.abs(res["dq"]).max() == 0.0
+    for si, keys in ((0, np.array([0, 1, 8191, 16384, 32767])), (1, np.array([0, 4095, 20000, 32767]))):
+        dk, dv = oracle.uniform_bwd_k0(f32(q), f32(kv[si][1]), Uo, f32(do), n, cu, q_segs, steps[si], keys)
+        assert_grad_close(res["dkv"][si][0][keys], dk, what=f"dK uniform step {si}")
+        assert_grad_close(res["dkv"][si][1][keys], dv, what=f"dV uniform step {si}")
+    assert np.abs(res["dkv"][2][0]).max() == 0.0 and np.abs(res["dkv"][2][1]).max() == 0.0
+
+
 @pytest.mark.parametrize("ds", [0, 1])
 def test_head_and_document_permutations_permute_the_outputs(ds):
     """Heads are independent and documents only see themselves: permuting the heads permutes

@@ -437,6 +437,10 @@ def main() -> int:
         # the same rate against the dense peak at the engine clock held during the timed region
         clock["pct_of_peak_at_measured_clock"] = (
             round(100 * value / (PEAK_BF16_TFLOPS * clock["held_mhz"] / 2400), 2) if clock["held_mhz"] else None)
+        if clock.get("mean_w") and clock["held_mhz"]:
+            # the device runs at its power limit: energy per step is what a step costs
+            clock["joules_per_step"] = round(clock["mean_w"] * ms_per_step / 1e3, 1)
+            clock["counted_tflop_per_joule"] = round(flop_step / 1e12 / (clock["mean_w"] * ms_per_step / 1e3), 4)
 
     out = {
         "metric": "causal attention TFLOP/s fwd+bwd per rank; % of MI355X bf16 MFMA peak",
